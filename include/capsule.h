@@ -1,0 +1,237 @@
+/*
+ * capsule.h -- execution-state capsules and the chunked gated linear-attention
+ * prefill scan, for one AMD Instinct MI355X (gfx950).  Plain C ABI.
+ *
+ * Source: "Execution-State Capsules: Graph-Bound Execution-State Checkpoint
+ * and Restore for Low-Latency, Small-Batch, On-Device Physical-AI Serving".
+ *
+ *   - A capsule freezes a committed boundary P of a closed, named set of live
+ *     device buffers (§3 "Definition"): positional full-attention KV valid
+ *     over [0, P), plus fixed-size state (linear-attention recurrent state,
+ *     convolution tails, other boundary state).
+ *   - snapshot / restore / fork / rollback are byte copies of that set
+ *     (§3 Algorithm 1 and "Four verbs"); snapshot chunk-aligns the boundary
+ *     to P' = floor(P / C) * C (§3 Algorithm 1; §5 "chunk-alignment
+ *     condition"); restore asserts the deployment digest first (§3
+ *     Algorithm 1) and rebinds the boundary.
+ *   - The robot episode reset is the same restore verb (§6); the batched form
+ *     here restores a per-environment capsule chosen from a gallery.
+ *   - The chunked scan is the recompute a capsule replaces (§3 Table "cost
+ *     structure", §3 "Cost model"); it folds its recurrent state once per
+ *     chunk (§5), which is what makes restore-at-P' followed by a prefill of
+ *     the remainder reproduce a cold prefill exactly.
+ *
+ * Conventions (§4: buffers are the only state primitive, the framework owns
+ * lifetime and pointers, copies are stream-ordered, errors are int returns;
+ * the contract is mechanism, never policy):
+ *   - Every device pointer is caller-owned (e.g. torch tensors).  The library
+ *     owns only host headers and the small static device segment table that
+ *     cap_set_create builds once per set.  No call below allocates device
+ *     memory except cap_set_create.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Device work is
+ *     asynchronous and stream-ordered; buffers and arenas must stay alive
+ *     until the stream has passed the call.
+ *   - Every function returns CAP_OK (0) or a negative CAP_E_* status.  All
+ *     argument checks run on the host first: on any error nothing has been
+ *     enqueued and no device byte has been written.
+ *   - Not thread-safe for concurrent calls on the same set or capsule.
+ */
+#ifndef CAPSULE_H
+#define CAPSULE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#if defined(__GNUC__)
+#define CAP_API __attribute__((visibility("default")))
+#else
+#define CAP_API
+#endif
+
+/* ------------------------------------------------------------ status ---- */
+#define CAP_OK              0
+#define CAP_E_INVAL        (-1)  /* null pointer, bad count/enum, overlapping buffers  */
+#define CAP_E_SIZE         (-2)  /* arena too small, layout mismatch, P beyond capacity */
+#define CAP_E_DIGEST       (-3)  /* prefix digest or deployment key mismatch           */
+#define CAP_E_UNSUPPORTED  (-4)  /* unknown buffer kind, unsupported shape or dtype    */
+#define CAP_E_ALIGN        (-5)  /* pointer or size not a multiple of 16 bytes         */
+#define CAP_E_STATE        (-6)  /* set position is not the aligned boundary           */
+#define CAP_E_HIP          (-7)  /* HIP runtime error (no device, allocation, launch)  */
+
+/* Static message for a status code (never NULL). */
+CAP_API const char* cap_status_string(int status);
+
+/* ----------------------------------------------------- buffer kinds ---- */
+/* CAP_KIND_POSITIONAL: a position-major buffer of `rows` rows of `row_bytes`
+ *   bytes (full-attention K or V, [T_max, kv_heads, d]); valid rows are the
+ *   prefix [0, P'), one contiguous byte range (§3 "Definition": the KV region
+ *   is valid over [0, P)).
+ * CAP_KIND_FIXED: a fixed-size buffer copied whole, row_bytes * rows bytes
+ *   (recurrent state, convolution tail, any other boundary state). */
+#define CAP_KIND_POSITIONAL 0u
+#define CAP_KIND_FIXED      1u
+
+#define CAP_DTYPE_F32  0
+#define CAP_DTYPE_BF16 1
+
+/* One named live buffer.  dptr: device pointer, 16-byte aligned, owned by the
+ * caller.  row_bytes: multiple of 16, > 0.  rows: > 0.  reserved: 0. */
+typedef struct cap_buf {
+    const char* name;      /* label (copied; may be NULL) */
+    void*       dptr;
+    uint64_t    row_bytes;
+    uint64_t    rows;
+    uint32_t    kind;      /* CAP_KIND_* */
+    uint32_t    reserved;
+} cap_buf;
+
+/* Limits of one call (host-checked; CAP_E_UNSUPPORTED beyond them). */
+#define CAP_MAX_BUFFERS 512u  /* buffers per set                   */
+#define CAP_MAX_FORK    16u   /* destination sets of one fork      */
+#define CAP_MAX_GALLERY 64u   /* capsules in one gather gallery    */
+
+typedef struct cap_set_s*     cap_set;      /* closed named live set           */
+typedef struct cap_capsule_s* cap_capsule;  /* host header of one capsule      */
+
+/* P' = floor(P / chunk) * chunk (§3 Algorithm 1); 0 when chunk == 0. */
+CAP_API uint64_t cap_align_boundary(uint64_t P, uint32_t chunk);
+
+/* Capsule bytes of a buffer list at boundary P (pure host; no device):
+ * sum over positional buffers of P' * row_bytes plus the bytes of every fixed
+ * buffer.  Same checks as cap_set_create except that dptr may be NULL. */
+CAP_API int capsule_layout_bytes(const cap_buf* bufs, uint32_t n, uint32_t chunk,
+                                 uint64_t P, uint64_t* bytes);
+
+/* Create a live set over n caller-owned buffers (the closed named buffer set
+ * B of §3 Algorithm 1), with chunk size `chunk` (>= 1) and a caller-chosen
+ * deployment key (a digest of weights, quantisation, kernels and shape
+ * bucket; restore refuses a capsule taken under another key, §3 Algorithm 1).
+ * Checks: names unique when given, kinds known, pointers and row_bytes
+ * 16-byte aligned, buffers pairwise disjoint.  Builds the static device
+ * segment table on the current device (one hipMalloc).  The set's position
+ * starts at 0.  *out receives the handle. */
+CAP_API int cap_set_create(const cap_buf* bufs, uint32_t n, uint32_t chunk,
+                           uint64_t deploy_key, cap_set* out);
+CAP_API int cap_set_destroy(cap_set set);
+
+/* Declare the boundary the live set currently holds: fixed buffers hold the
+ * state after `position` tokens and positional buffers are valid over
+ * [0, position).  Must not exceed the capacity (rows) of any positional
+ * buffer (CAP_E_SIZE). */
+CAP_API int cap_set_set_position(cap_set set, uint64_t position);
+CAP_API int cap_set_get_position(cap_set set, uint64_t* position);
+
+/* Capsule bytes of this set at boundary P (P is aligned first). */
+CAP_API int capsule_bytes(cap_set set, uint64_t P, uint64_t* bytes);
+
+/* snapshot(P) (§3 Algorithm 1): P' = floor(P / C) * C; the set's position
+ * must equal P' (CAP_E_STATE otherwise -- the fixed buffers must hold the
+ * state at P', e.g. from a prefill that stopped at P' or from the scan's
+ * chunk-boundary state output); P' must fit every positional buffer
+ * (CAP_E_SIZE).  Copies the set, valid at P', into `arena` (device,
+ * caller-owned, 16-byte aligned, >= capsule_bytes, disjoint from every live
+ * buffer) in one launch: buffers in set order, positional buffers
+ * contributing rows [0, P'), fixed buffers all their bytes.  *out receives a
+ * host header {P', prefix_digest, deploy key, layout}; the arena stays the
+ * caller's and must outlive the header's use. */
+CAP_API int capsule_snapshot(cap_set live, uint64_t P, uint64_t prefix_digest,
+                             void* arena, uint64_t arena_bytes, void* stream,
+                             cap_capsule* out);
+
+/* restore (§3 Algorithm 1; rollback is a restore of an earlier capsule):
+ * checks, in order, the prefix digest and the set's deployment key
+ * (CAP_E_DIGEST), then that the set's layout equals the capsule's
+ * (CAP_E_SIZE); then copies the arena back into the live buffers in one
+ * launch and rebinds the boundary: the set's position becomes P' (returned
+ * in *P_restored, which may be NULL).  Positional rows at or beyond P' are
+ * not written. */
+CAP_API int capsule_restore(cap_capsule cap, cap_set live, uint64_t prefix_digest,
+                            void* stream, uint64_t* P_restored);
+
+/* fork 1 -> n (§3 "Four verbs", Algorithm 1 fork): restore one capsule into n
+ * distinct live sets (1 <= n <= CAP_MAX_FORK) in one launch that reads each
+ * capsule byte once and writes it n times.  Same checks as restore, for every
+ * set; every set's position becomes P'. */
+CAP_API int capsule_fork(cap_capsule cap, const cap_set* lives, uint32_t n,
+                         uint64_t prefix_digest, void* stream);
+
+/* Batched episode reset (§6: reset is a restore of a boundary capsule):
+ * environment e in [0, n_env) receives a restore of gallery[ids[e]].  ids is
+ * a HOST array of n_env int32 in [0, n_gallery) (CAP_E_INVAL otherwise).
+ * All gallery capsules and all environment sets must share one layout and
+ * one P' and deployment key (CAP_E_SIZE / CAP_E_DIGEST); the env sets must be
+ * distinct.  One launch per call for any n_env; every env set's position
+ * becomes P'. */
+CAP_API int capsule_gather_restore(const cap_capsule* gallery, uint32_t n_gallery,
+                                   const int32_t* ids, const cap_set* lives,
+                                   uint32_t n_env, void* stream);
+
+/* Header fields of a capsule (any output pointer may be NULL). */
+CAP_API int capsule_info(cap_capsule cap, uint64_t* P_aligned, uint64_t* bytes,
+                         uint64_t* prefix_digest, uint64_t* deploy_key,
+                         const void** arena);
+
+/* Free the host header (the arena remains the caller's). */
+CAP_API int capsule_release(cap_capsule cap);
+
+/* Token-prefix digest for the boundary descriptor (§3 Algorithm 1 names one
+ * without fixing the function): 64-bit FNV-1a over the little-endian bytes
+ * of n int32 token ids (host). */
+CAP_API uint64_t capsule_digest_tokens(const int32_t* ids, uint64_t n);
+
+/* ------------------------------------- chunked linear-attention prefill -- */
+/* Gated linear attention, per head h (state dk x dv, §2 "hybrid recurrent
+ * state": a fold over the whole prefix):
+ *     S_t = exp(g_t) * S_{t-1} + k_t^T v_t,      o_t = scale * q_t S_t
+ * computed in chunks of C tokens counted from the first token of the call
+ * (§5: the state is folded once per chunk).  For chunk j with entering state
+ * S_j and inclusive in-chunk log-decay sums G_i:
+ *     o_i     = scale * (exp(G_i) q_i S_j + sum_{m<=i} exp(G_i - G_m) (q_i.k_m) v_m)
+ *     S_{j+1} = exp(G_last) S_j + sum_m exp(G_last - G_m) k_m^T v_m
+ * The arithmetic of a chunk depends only on (S_j, that chunk's inputs): a
+ * call started at a chunk-aligned position from a restored state reproduces,
+ * bit for bit, what one longer call computes for the same tokens.
+ *
+ * Layouts (all contiguous, device, caller-owned):
+ *   q, k : [T, H, dk]  in_dtype (bf16 or f32)      v : [T, H, dv] in_dtype
+ *   g    : [T, H] fp32 log-gates, finite (normally <= 0)
+ *   state_in     : [H, dk, dv] fp32, or NULL for a zero state
+ *   o            : [T, H, dv] fp32 (written for every token)
+ *   chunk_states : [ceil(T/C), H, dk, dv] fp32 or NULL; entry j is the state
+ *                  ENTERING chunk j (entry 0 = state_in)
+ *   final_state  : [H, dk, dv] fp32 or NULL; the state after the last token.
+ *                  May be the same pointer as state_in (in-place update).
+ * Supported: chunk == 64, dk in {64, 128} (fp32 inputs: dk == 64), dv a
+ * multiple of 16, 1 <= H,
+ * 0 <= T; pointers 16-byte aligned; o / chunk_states / final_state must not
+ * overlap the inputs (except final_state == state_in).
+ * Errors: CAP_E_INVAL (null required pointer, T < 0, H < 1, bad dtype,
+ * overlap), CAP_E_UNSUPPORTED (shape outside the list), CAP_E_ALIGN. */
+typedef struct linattn_args {
+    const void*  q;
+    const void*  k;
+    const void*  v;
+    const float* g;
+    const float* state_in;
+    float*       o;
+    float*       chunk_states;
+    float*       final_state;
+    int64_t      T;
+    int32_t      H;
+    int32_t      dk;
+    int32_t      dv;
+    int32_t      chunk;
+    int32_t      in_dtype;   /* CAP_DTYPE_BF16 or CAP_DTYPE_F32 */
+    float        scale;
+} linattn_args;
+
+CAP_API int linattn_chunked_prefill(const linattn_args* args, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CAPSULE_H */

@@ -1,0 +1,275 @@
+"""ctypes binding of libcapsule.so: argument marshalling only.
+
+Every function here has the name of the C entry point it calls (include/
+capsule.h) and forwards to it; all work runs in the library's HIP kernels.
+Device buffers are passed as torch tensors (their data pointers) or as raw
+integer addresses; streams as torch streams, raw hipStream_t integers or
+None (torch's current stream).  A non-zero status raises CapsuleError.
+There is no fallback: if the library is missing, loading raises.
+"""
+import ctypes as ct
+import os
+
+from .build import LIB_PATH
+
+CAP_OK = 0
+CAP_E_INVAL = -1
+CAP_E_SIZE = -2
+CAP_E_DIGEST = -3
+CAP_E_UNSUPPORTED = -4
+CAP_E_ALIGN = -5
+CAP_E_STATE = -6
+CAP_E_HIP = -7
+
+CAP_KIND_POSITIONAL = 0
+CAP_KIND_FIXED = 1
+CAP_DTYPE_F32 = 0
+CAP_DTYPE_BF16 = 1
+
+CAP_MAX_BUFFERS = 512
+CAP_MAX_FORK = 16
+CAP_MAX_GALLERY = 64
+
+
+class CapsuleError(RuntimeError):
+    def __init__(self, fn, status, msg):
+        super().__init__("%s failed: %d (%s)" % (fn, status, msg))
+        self.status = status
+        self.fn = fn
+
+
+class cap_buf(ct.Structure):
+    _fields_ = [("name", ct.c_char_p), ("dptr", ct.c_void_p), ("row_bytes", ct.c_uint64),
+                ("rows", ct.c_uint64), ("kind", ct.c_uint32), ("reserved", ct.c_uint32)]
+
+
+class linattn_args(ct.Structure):
+    _fields_ = [("q", ct.c_void_p), ("k", ct.c_void_p), ("v", ct.c_void_p), ("g", ct.c_void_p),
+                ("state_in", ct.c_void_p), ("o", ct.c_void_p), ("chunk_states", ct.c_void_p),
+                ("final_state", ct.c_void_p), ("T", ct.c_int64), ("H", ct.c_int32), ("dk", ct.c_int32),
+                ("dv", ct.c_int32), ("chunk", ct.c_int32), ("in_dtype", ct.c_int32), ("scale", ct.c_float)]
+
+
+# (name, restype, argtypes) of every exported entry point
+_vp, _u64, _u32, _i32 = ct.c_void_p, ct.c_uint64, ct.c_uint32, ct.c_int32
+SIGNATURES = [
+    ("cap_status_string", ct.c_char_p, [ct.c_int]),
+    ("cap_align_boundary", _u64, [_u64, _u32]),
+    ("capsule_layout_bytes", ct.c_int, [ct.POINTER(cap_buf), _u32, _u32, _u64, ct.POINTER(_u64)]),
+    ("cap_set_create", ct.c_int, [ct.POINTER(cap_buf), _u32, _u32, _u64, ct.POINTER(_vp)]),
+    ("cap_set_destroy", ct.c_int, [_vp]),
+    ("cap_set_set_position", ct.c_int, [_vp, _u64]),
+    ("cap_set_get_position", ct.c_int, [_vp, ct.POINTER(_u64)]),
+    ("capsule_bytes", ct.c_int, [_vp, _u64, ct.POINTER(_u64)]),
+    ("capsule_snapshot", ct.c_int, [_vp, _u64, _u64, _vp, _u64, _vp, ct.POINTER(_vp)]),
+    ("capsule_restore", ct.c_int, [_vp, _vp, _u64, _vp, ct.POINTER(_u64)]),
+    ("capsule_fork", ct.c_int, [_vp, ct.POINTER(_vp), _u32, _u64, _vp]),
+    ("capsule_gather_restore", ct.c_int, [ct.POINTER(_vp), _u32, ct.POINTER(_i32), ct.POINTER(_vp), _u32, _vp]),
+    ("capsule_info", ct.c_int, [_vp, ct.POINTER(_u64), ct.POINTER(_u64), ct.POINTER(_u64), ct.POINTER(_u64),
+                                ct.POINTER(_vp)]),
+    ("capsule_release", ct.c_int, [_vp]),
+    ("capsule_digest_tokens", _u64, [ct.POINTER(_i32), _u64]),
+    ("linattn_chunked_prefill", ct.c_int, [ct.POINTER(linattn_args), _vp]),
+]
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Load libcapsule.so (built by ``paper_2606_20537_amd.build``)."""
+    global _lib
+    if _lib is not None and path == LIB_PATH:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError("libcapsule.so is not built (%s); run paper_2606_20537_amd.build.build()" % path)
+    lib = ct.CDLL(path)
+    for name, res, args in SIGNATURES:
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    if path == LIB_PATH:
+        _lib = lib
+    return lib
+
+
+def _check(fn, status):
+    if status != CAP_OK:
+        raise CapsuleError(fn, status, load().cap_status_string(status).decode())
+    return status
+
+
+def _addr(x):
+    """Device address of a torch tensor or an int (None -> 0)."""
+    if x is None:
+        return 0
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(s):
+    if s is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(s, int):
+        return s
+    return s.cuda_stream
+
+
+class CapSet:
+    """Handle of a live set (owns the C handle; destroy() or GC frees it)."""
+
+    def __init__(self, handle, names, n):
+        self.handle = handle
+        self.names = names
+        self.n = n
+
+    def destroy(self):
+        if self.handle:
+            cap_set_destroy(self)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass
+
+
+class Capsule:
+    """Host header of one capsule; the arena is the caller's."""
+
+    def __init__(self, handle, arena_ref):
+        self.handle = handle
+        self.arena_ref = arena_ref  # keeps a torch arena alive while the header lives
+
+    def release(self):
+        if self.handle:
+            capsule_release(self)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.release()
+        except Exception:
+            pass
+
+
+def make_bufs(bufs):
+    """bufs: iterable of (name, tensor_or_addr, row_bytes, rows, kind)."""
+    bufs = list(bufs)
+    arr = (cap_buf * len(bufs))()
+    keep = []
+    for i, (name, t, rb, rows, kind) in enumerate(bufs):
+        nb = name.encode() if name is not None else None
+        keep.append(nb)
+        arr[i] = cap_buf(nb, _addr(t), int(rb), int(rows), int(kind), 0)
+    return arr, keep
+
+
+# ------------------------------------------------------------ entry points --
+def cap_status_string(status):
+    return load().cap_status_string(int(status)).decode()
+
+
+def cap_align_boundary(P, chunk):
+    return int(load().cap_align_boundary(int(P), int(chunk)))
+
+
+def capsule_layout_bytes(bufs, chunk, P):
+    arr, _keep = make_bufs(bufs)
+    out = _u64(0)
+    _check("capsule_layout_bytes", load().capsule_layout_bytes(arr, len(arr), int(chunk), int(P), ct.byref(out)))
+    return int(out.value)
+
+
+def cap_set_create(bufs, chunk, deploy_key):
+    arr, keep = make_bufs(bufs)
+    h = _vp()
+    _check("cap_set_create", load().cap_set_create(arr, len(arr), int(chunk), int(deploy_key) & (2**64 - 1),
+                                                    ct.byref(h)))
+    return CapSet(h.value, [k.decode() if k else None for k in keep], len(arr))
+
+
+def cap_set_destroy(s):
+    return _check("cap_set_destroy", load().cap_set_destroy(s.handle))
+
+
+def cap_set_set_position(s, position):
+    return _check("cap_set_set_position", load().cap_set_set_position(s.handle, int(position)))
+
+
+def cap_set_get_position(s):
+    out = _u64(0)
+    _check("cap_set_get_position", load().cap_set_get_position(s.handle, ct.byref(out)))
+    return int(out.value)
+
+
+def capsule_bytes(s, P):
+    out = _u64(0)
+    _check("capsule_bytes", load().capsule_bytes(s.handle, int(P), ct.byref(out)))
+    return int(out.value)
+
+
+def capsule_snapshot(s, P, prefix_digest, arena, arena_bytes=None, stream=None):
+    if arena_bytes is None:
+        arena_bytes = arena.numel() * arena.element_size()
+    h = _vp()
+    _check("capsule_snapshot", load().capsule_snapshot(s.handle, int(P), int(prefix_digest) & (2**64 - 1),
+                                                        _addr(arena), int(arena_bytes), _stream(stream),
+                                                        ct.byref(h)))
+    return Capsule(h.value, arena)
+
+
+def capsule_restore(cap, s, prefix_digest, stream=None):
+    out = _u64(0)
+    _check("capsule_restore", load().capsule_restore(cap.handle, s.handle, int(prefix_digest) & (2**64 - 1),
+                                                      _stream(stream), ct.byref(out)))
+    return int(out.value)
+
+
+def capsule_fork(cap, sets, prefix_digest, stream=None):
+    arr = (_vp * len(sets))(*[s.handle for s in sets])
+    return _check("capsule_fork", load().capsule_fork(cap.handle, arr, len(sets), int(prefix_digest) & (2**64 - 1),
+                                                      _stream(stream)))
+
+
+def capsule_gather_restore(gallery, ids, sets, stream=None):
+    gal = (_vp * len(gallery))(*[c.handle for c in gallery])
+    ids_arr = (_i32 * len(ids))(*[int(i) for i in ids])
+    arr = (_vp * len(sets))(*[s.handle for s in sets])
+    return _check("capsule_gather_restore", load().capsule_gather_restore(gal, len(gallery), ids_arr, arr,
+                                                                          len(sets), _stream(stream)))
+
+
+def capsule_info(cap):
+    P, nb, pd, dk, ar = _u64(0), _u64(0), _u64(0), _u64(0), _vp()
+    _check("capsule_info", load().capsule_info(cap.handle, ct.byref(P), ct.byref(nb), ct.byref(pd), ct.byref(dk),
+                                               ct.byref(ar)))
+    return {"P_aligned": int(P.value), "bytes": int(nb.value), "prefix_digest": int(pd.value),
+            "deploy_key": int(dk.value), "arena": int(ar.value or 0)}
+
+
+def capsule_release(cap):
+    return _check("capsule_release", load().capsule_release(cap.handle))
+
+
+def capsule_digest_tokens(ids):
+    import numpy as np
+    a = np.ascontiguousarray(ids, dtype=np.int32)
+    return int(load().capsule_digest_tokens(a.ctypes.data_as(ct.POINTER(_i32)), a.size))
+
+
+def linattn_chunked_prefill(q, k, v, g, o, *, state_in=None, chunk_states=None, final_state=None,
+                            T=None, H=None, dk=None, dv=None, chunk=64, in_dtype=None, scale=1.0,
+                            stream=None):
+    """Marshal tensors (or addresses with explicit sizes) into linattn_args."""
+    if T is None:
+        T, H, dk = q.shape
+        dv = v.shape[2]
+    if in_dtype is None:
+        import torch
+        in_dtype = CAP_DTYPE_F32 if q.dtype == torch.float32 else CAP_DTYPE_BF16
+    a = linattn_args(_addr(q), _addr(k), _addr(v), _addr(g), _addr(state_in), _addr(o), _addr(chunk_states),
+                     _addr(final_state), int(T), int(H), int(dk), int(dv), int(chunk), int(in_dtype), float(scale))
+    return _check("linattn_chunked_prefill", load().linattn_chunked_prefill(ct.byref(a), _stream(stream)))

@@ -1,0 +1,471 @@
+// Host side of the capsule C ABI: live sets, capsule headers, argument
+// checks and kernel launches.  Every check runs before anything is enqueued,
+// so an error return leaves device memory untouched (paper §4: the contract
+// is mechanism only and reports errors as int status codes; §3 Algorithm 1:
+// restore asserts the deployment digest before copying).
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "capsule.h"
+#include "internal.h"
+
+using cap::SegEntry;
+
+struct BufInfo {
+    std::string name;
+    uint64_t ptr;
+    uint64_t row_bytes;
+    uint64_t rows;
+    uint32_t kind;
+};
+
+struct cap_set_s {
+    std::vector<BufInfo> bufs;
+    uint32_t chunk = 1;
+    uint64_t deploy_key = 0;
+    uint64_t position = 0;
+    uint64_t max_position = 0;  // smallest positional capacity (UINT64_MAX if none)
+    SegEntry* dtab = nullptr;   // n + 1 entries on the device
+    int device = 0;
+    int num_cus = 256;
+};
+
+struct cap_capsule_s {
+    uint64_t P_requested = 0;
+    uint64_t P_aligned = 0;
+    uint64_t prefix_digest = 0;
+    uint64_t deploy_key = 0;
+    uint64_t bytes = 0;
+    const void* arena = nullptr;
+    uint64_t arena_bytes = 0;
+    std::vector<uint64_t> row_bytes, rows;
+    std::vector<uint32_t> kinds;
+};
+
+namespace {
+
+bool aligned16(uint64_t x) { return (x & 15u) == 0; }
+
+uint64_t buf_bytes(uint64_t row_bytes, uint64_t rows, uint32_t kind, uint64_t P) {
+    return kind == CAP_KIND_POSITIONAL ? P * row_bytes : row_bytes * rows;
+}
+
+// Shared checks of a buffer list.  need_ptr: device pointers must be set.
+int check_bufs(const cap_buf* bufs, uint32_t n, uint32_t chunk, bool need_ptr) {
+    if (!bufs || n == 0) return CAP_E_INVAL;
+    if (n > CAP_MAX_BUFFERS) return CAP_E_UNSUPPORTED;
+    if (chunk == 0) return CAP_E_INVAL;
+    for (uint32_t i = 0; i < n; ++i) {
+        const cap_buf& b = bufs[i];
+        if (b.kind != CAP_KIND_POSITIONAL && b.kind != CAP_KIND_FIXED) return CAP_E_UNSUPPORTED;
+        if (b.reserved != 0) return CAP_E_INVAL;
+        if (b.row_bytes == 0 || b.rows == 0) return CAP_E_INVAL;
+        if (b.row_bytes > (UINT64_MAX / b.rows)) return CAP_E_SIZE;
+        if (need_ptr && !b.dptr) return CAP_E_INVAL;
+        if (!aligned16(b.row_bytes) || !aligned16((uint64_t)(uintptr_t)b.dptr)) return CAP_E_ALIGN;
+    }
+    // unique names (when given)
+    std::vector<std::string> names;
+    for (uint32_t i = 0; i < n; ++i)
+        if (bufs[i].name) names.emplace_back(bufs[i].name);
+    std::sort(names.begin(), names.end());
+    if (std::adjacent_find(names.begin(), names.end()) != names.end()) return CAP_E_INVAL;
+    if (need_ptr) {  // pairwise disjoint
+        std::vector<std::pair<uint64_t, uint64_t>> r;
+        for (uint32_t i = 0; i < n; ++i) {
+            const uint64_t p = (uint64_t)(uintptr_t)bufs[i].dptr;
+            r.emplace_back(p, p + bufs[i].row_bytes * bufs[i].rows);
+        }
+        std::sort(r.begin(), r.end());
+        for (size_t i = 1; i < r.size(); ++i)
+            if (r[i].first < r[i - 1].second) return CAP_E_INVAL;
+    }
+    return CAP_OK;
+}
+
+bool overlaps(uint64_t a0, uint64_t a1, uint64_t b0, uint64_t b1) { return a0 < b1 && b0 < a1; }
+
+int current_device_matches(const cap_set_s* s) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return CAP_E_HIP;
+    return dev == s->device ? CAP_OK : CAP_E_INVAL;
+}
+
+bool same_layout(const cap_capsule_s* c, const cap_set_s* s) {
+    if (c->kinds.size() != s->bufs.size()) return false;
+    for (size_t i = 0; i < s->bufs.size(); ++i)
+        if (c->row_bytes[i] != s->bufs[i].row_bytes || c->rows[i] != s->bufs[i].rows ||
+            c->kinds[i] != s->bufs[i].kind)
+            return false;
+    return true;
+}
+
+// restore-side checks shared by restore, fork and gather (digest first).
+int check_restore_target(const cap_capsule_s* c, const cap_set_s* s, uint64_t prefix_digest, bool check_prefix) {
+    if (check_prefix && c->prefix_digest != prefix_digest) return CAP_E_DIGEST;
+    if (c->deploy_key != s->deploy_key) return CAP_E_DIGEST;
+    if (!same_layout(c, s)) return CAP_E_SIZE;
+    if (c->P_aligned > s->max_position) return CAP_E_SIZE;
+    const uint64_t a0 = (uint64_t)(uintptr_t)c->arena, a1 = a0 + c->bytes;
+    for (const BufInfo& b : s->bufs)
+        if (overlaps(a0, a1, b.ptr, b.ptr + b.row_bytes * b.rows)) return CAP_E_INVAL;
+    return CAP_OK;
+}
+
+int launch_status(hipError_t e) { return e == hipSuccess ? CAP_OK : CAP_E_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+const char* cap_status_string(int status) {
+    switch (status) {
+        case CAP_OK: return "ok";
+        case CAP_E_INVAL: return "invalid argument";
+        case CAP_E_SIZE: return "size or layout mismatch";
+        case CAP_E_DIGEST: return "digest or deployment key mismatch";
+        case CAP_E_UNSUPPORTED: return "unsupported kind, shape or dtype";
+        case CAP_E_ALIGN: return "pointer or size not 16-byte aligned";
+        case CAP_E_STATE: return "set position is not the aligned boundary";
+        case CAP_E_HIP: return "HIP runtime error";
+        default: return "unknown status";
+    }
+}
+
+uint64_t cap_align_boundary(uint64_t P, uint32_t chunk) {
+    return chunk ? (P / chunk) * (uint64_t)chunk : 0;
+}
+
+int capsule_layout_bytes(const cap_buf* bufs, uint32_t n, uint32_t chunk, uint64_t P, uint64_t* bytes) {
+    if (!bytes) return CAP_E_INVAL;
+    const int rc = check_bufs(bufs, n, chunk, false);
+    if (rc != CAP_OK) return rc;
+    const uint64_t Pa = cap_align_boundary(P, chunk);
+    uint64_t total = 0;
+    for (uint32_t i = 0; i < n; ++i) {
+        if (bufs[i].kind == CAP_KIND_POSITIONAL && Pa > bufs[i].rows) return CAP_E_SIZE;
+        total += buf_bytes(bufs[i].row_bytes, bufs[i].rows, bufs[i].kind, Pa);
+    }
+    *bytes = total;
+    return CAP_OK;
+}
+
+int cap_set_create(const cap_buf* bufs, uint32_t n, uint32_t chunk, uint64_t deploy_key, cap_set* out) {
+    if (!out) return CAP_E_INVAL;
+    *out = nullptr;
+    int rc = check_bufs(bufs, n, chunk, true);
+    if (rc != CAP_OK) return rc;
+
+    cap_set_s* s = new (std::nothrow) cap_set_s();
+    if (!s) return CAP_E_INVAL;
+    s->chunk = chunk;
+    s->deploy_key = deploy_key;
+    s->max_position = UINT64_MAX;
+    std::vector<SegEntry> tab(n + 1);
+    uint64_t a = 0, b = 0;
+    for (uint32_t i = 0; i < n; ++i) {
+        BufInfo bi{bufs[i].name ? bufs[i].name : std::string(), (uint64_t)(uintptr_t)bufs[i].dptr,
+                   bufs[i].row_bytes, bufs[i].rows, bufs[i].kind};
+        s->bufs.push_back(bi);
+        tab[i] = SegEntry{bi.ptr, a, b};
+        if (bi.kind == CAP_KIND_POSITIONAL) {
+            b += bi.row_bytes;
+            s->max_position = std::min(s->max_position, bi.rows);
+        } else {
+            a += bi.row_bytes * bi.rows;
+        }
+    }
+    tab[n] = SegEntry{0, a, b};
+
+    if (hipGetDevice(&s->device) != hipSuccess) { delete s; return CAP_E_HIP; }
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, s->device) == hipSuccess && cus > 0)
+        s->num_cus = cus;
+    void* d = nullptr;
+    if (hipMalloc(&d, sizeof(SegEntry) * (n + 1)) != hipSuccess) { delete s; return CAP_E_HIP; }
+    if (hipMemcpy(d, tab.data(), sizeof(SegEntry) * (n + 1), hipMemcpyHostToDevice) != hipSuccess) {
+        (void)hipFree(d);
+        delete s;
+        return CAP_E_HIP;
+    }
+    s->dtab = static_cast<SegEntry*>(d);
+    *out = s;
+    return CAP_OK;
+}
+
+int cap_set_destroy(cap_set set) {
+    if (!set) return CAP_E_INVAL;
+    if (set->dtab) (void)hipFree(set->dtab);
+    delete set;
+    return CAP_OK;
+}
+
+int cap_set_set_position(cap_set set, uint64_t position) {
+    if (!set) return CAP_E_INVAL;
+    if (position > set->max_position) return CAP_E_SIZE;
+    set->position = position;
+    return CAP_OK;
+}
+
+int cap_set_get_position(cap_set set, uint64_t* position) {
+    if (!set || !position) return CAP_E_INVAL;
+    *position = set->position;
+    return CAP_OK;
+}
+
+int capsule_bytes(cap_set set, uint64_t P, uint64_t* bytes) {
+    if (!set || !bytes) return CAP_E_INVAL;
+    const uint64_t Pa = cap_align_boundary(P, set->chunk);
+    if (Pa > set->max_position) return CAP_E_SIZE;
+    uint64_t total = 0;
+    for (const BufInfo& b : set->bufs) total += buf_bytes(b.row_bytes, b.rows, b.kind, Pa);
+    *bytes = total;
+    return CAP_OK;
+}
+
+int capsule_snapshot(cap_set live, uint64_t P, uint64_t prefix_digest, void* arena, uint64_t arena_bytes,
+                     void* stream, cap_capsule* out) {
+    if (!out) return CAP_E_INVAL;
+    *out = nullptr;
+    if (!live || !arena) return CAP_E_INVAL;
+    if (!aligned16((uint64_t)(uintptr_t)arena)) return CAP_E_ALIGN;
+    const uint64_t Pa = cap_align_boundary(P, live->chunk);
+    if (Pa > live->max_position) return CAP_E_SIZE;
+    if (live->position != Pa) return CAP_E_STATE;
+    uint64_t bytes = 0;
+    capsule_bytes(live, P, &bytes);
+    if (arena_bytes < bytes) return CAP_E_SIZE;
+    const uint64_t a0 = (uint64_t)(uintptr_t)arena, a1 = a0 + bytes;
+    for (const BufInfo& b : live->bufs)
+        if (overlaps(a0, a1, b.ptr, b.ptr + b.row_bytes * b.rows)) return CAP_E_INVAL;
+    int rc = current_device_matches(live);
+    if (rc != CAP_OK) return rc;
+
+    cap_capsule_s* c = new (std::nothrow) cap_capsule_s();
+    if (!c) return CAP_E_INVAL;
+    c->P_requested = P;
+    c->P_aligned = Pa;
+    c->prefix_digest = prefix_digest;
+    c->deploy_key = live->deploy_key;
+    c->bytes = bytes;
+    c->arena = arena;
+    c->arena_bytes = arena_bytes;
+    for (const BufInfo& b : live->bufs) {
+        c->row_bytes.push_back(b.row_bytes);
+        c->rows.push_back(b.rows);
+        c->kinds.push_back(b.kind);
+    }
+
+    cap::CopyParams p{};
+    p.layout = live->dtab;
+    p.tabs[0] = live->dtab;
+    p.arena_out = static_cast<uint8_t*>(arena);
+    p.P = Pa;
+    p.nvec = bytes / 16;
+    p.n_seg = (uint32_t)live->bufs.size();
+    p.n_dst = 1;
+    p.n_rep = 1;
+    p.mode = cap::kLiveToArena;
+    rc = launch_status(cap::launch_copy(p, live->num_cus, static_cast<hipStream_t>(stream)));
+    if (rc != CAP_OK) { delete c; return rc; }
+    *out = c;
+    return CAP_OK;
+}
+
+int capsule_restore(cap_capsule cap, cap_set live, uint64_t prefix_digest, void* stream, uint64_t* P_restored) {
+    if (!cap || !live) return CAP_E_INVAL;
+    int rc = check_restore_target(cap, live, prefix_digest, true);
+    if (rc != CAP_OK) return rc;
+    rc = current_device_matches(live);
+    if (rc != CAP_OK) return rc;
+    cap::CopyParams p{};
+    p.layout = live->dtab;
+    p.tabs[0] = live->dtab;
+    p.arena_in[0] = static_cast<const uint8_t*>(cap->arena);
+    p.P = cap->P_aligned;
+    p.nvec = cap->bytes / 16;
+    p.n_seg = (uint32_t)live->bufs.size();
+    p.n_dst = 1;
+    p.n_rep = 1;
+    p.mode = cap::kArenaToLive;
+    rc = launch_status(cap::launch_copy(p, live->num_cus, static_cast<hipStream_t>(stream)));
+    if (rc != CAP_OK) return rc;
+    live->position = cap->P_aligned;
+    if (P_restored) *P_restored = cap->P_aligned;
+    return CAP_OK;
+}
+
+int capsule_fork(cap_capsule cap, const cap_set* lives, uint32_t n, uint64_t prefix_digest, void* stream) {
+    if (!cap || !lives || n == 0) return CAP_E_INVAL;
+    if (n > CAP_MAX_FORK) return CAP_E_UNSUPPORTED;
+    for (uint32_t i = 0; i < n; ++i) {
+        if (!lives[i]) return CAP_E_INVAL;
+        for (uint32_t j = 0; j < i; ++j)
+            if (lives[j] == lives[i]) return CAP_E_INVAL;
+    }
+    for (uint32_t i = 0; i < n; ++i) {
+        const int rc = check_restore_target(cap, lives[i], prefix_digest, true);
+        if (rc != CAP_OK) return rc;
+        if (lives[i]->device != lives[0]->device) return CAP_E_INVAL;
+    }
+    int rc = current_device_matches(lives[0]);
+    if (rc != CAP_OK) return rc;
+    // destinations per launch bounded by the kernel's LDS pointer table
+    const uint32_t n_seg = (uint32_t)lives[0]->bufs.size();
+    const uint32_t per_launch = std::max<uint32_t>(1, std::min<uint32_t>(cap::kMaxDst, (uint32_t)cap::kMaxPtrLds / n_seg));
+    for (uint32_t first = 0; first < n; first += per_launch) {
+        const uint32_t cnt = std::min(per_launch, n - first);
+        cap::CopyParams p{};
+        p.layout = lives[first]->dtab;
+        for (uint32_t d = 0; d < cnt; ++d) p.tabs[d] = lives[first + d]->dtab;
+        p.arena_in[0] = static_cast<const uint8_t*>(cap->arena);
+        p.P = cap->P_aligned;
+        p.nvec = cap->bytes / 16;
+        p.n_seg = n_seg;
+        p.n_dst = cnt;
+        p.n_rep = 1;
+        p.mode = cap::kArenaToLive;
+        rc = launch_status(cap::launch_copy(p, lives[0]->num_cus, static_cast<hipStream_t>(stream)));
+        if (rc != CAP_OK) return rc;
+    }
+    for (uint32_t i = 0; i < n; ++i) lives[i]->position = cap->P_aligned;
+    return CAP_OK;
+}
+
+int capsule_gather_restore(const cap_capsule* gallery, uint32_t n_gallery, const int32_t* ids,
+                           const cap_set* lives, uint32_t n_env, void* stream) {
+    if (!gallery || !ids || !lives || n_gallery == 0 || n_env == 0) return CAP_E_INVAL;
+    if (n_gallery > CAP_MAX_GALLERY) return CAP_E_UNSUPPORTED;
+    for (uint32_t gi = 0; gi < n_gallery; ++gi)
+        if (!gallery[gi]) return CAP_E_INVAL;
+    for (uint32_t e = 0; e < n_env; ++e) {
+        if (!lives[e]) return CAP_E_INVAL;
+        if (ids[e] < 0 || (uint32_t)ids[e] >= n_gallery) return CAP_E_INVAL;
+    }
+    {   // distinct environment sets
+        std::vector<cap_set> v(lives, lives + n_env);
+        std::sort(v.begin(), v.end());
+        if (std::adjacent_find(v.begin(), v.end()) != v.end()) return CAP_E_INVAL;
+    }
+    const cap_capsule_s* c0 = gallery[0];
+    for (uint32_t gi = 1; gi < n_gallery; ++gi) {
+        const cap_capsule_s* c = gallery[gi];
+        if (c->deploy_key != c0->deploy_key) return CAP_E_DIGEST;
+        if (c->P_aligned != c0->P_aligned || c->bytes != c0->bytes || c->kinds != c0->kinds ||
+            c->row_bytes != c0->row_bytes || c->rows != c0->rows)
+            return CAP_E_SIZE;
+    }
+    for (uint32_t e = 0; e < n_env; ++e) {
+        // every gallery arena is checked against every env set for overlap
+        for (uint32_t gi = 0; gi < n_gallery; ++gi) {
+            const int rc = check_restore_target(gallery[gi], lives[e], 0, false);
+            if (rc != CAP_OK) return rc;
+        }
+        if (lives[e]->device != lives[0]->device) return CAP_E_INVAL;
+    }
+    int rc = current_device_matches(lives[0]);
+    if (rc != CAP_OK) return rc;
+    const uint32_t n_seg = (uint32_t)lives[0]->bufs.size();
+    for (uint32_t first = 0; first < n_env; first += cap::kMaxRep) {
+        const uint32_t cnt = std::min<uint32_t>(cap::kMaxRep, n_env - first);
+        cap::CopyParams p{};
+        p.layout = lives[first]->dtab;
+        for (uint32_t r = 0; r < cnt; ++r) {
+            p.tabs[r] = lives[first + r]->dtab;
+            p.arena_in[r] = static_cast<const uint8_t*>(gallery[ids[first + r]]->arena);
+        }
+        p.P = c0->P_aligned;
+        p.nvec = c0->bytes / 16;
+        p.n_seg = n_seg;
+        p.n_dst = 1;
+        p.n_rep = cnt;
+        p.mode = cap::kArenaToLive;
+        rc = launch_status(cap::launch_copy(p, lives[0]->num_cus, static_cast<hipStream_t>(stream)));
+        if (rc != CAP_OK) return rc;
+    }
+    for (uint32_t e = 0; e < n_env; ++e) lives[e]->position = c0->P_aligned;
+    return CAP_OK;
+}
+
+int capsule_info(cap_capsule cap, uint64_t* P_aligned, uint64_t* bytes, uint64_t* prefix_digest,
+                 uint64_t* deploy_key, const void** arena) {
+    if (!cap) return CAP_E_INVAL;
+    if (P_aligned) *P_aligned = cap->P_aligned;
+    if (bytes) *bytes = cap->bytes;
+    if (prefix_digest) *prefix_digest = cap->prefix_digest;
+    if (deploy_key) *deploy_key = cap->deploy_key;
+    if (arena) *arena = cap->arena;
+    return CAP_OK;
+}
+
+int capsule_release(cap_capsule cap) {
+    if (!cap) return CAP_E_INVAL;
+    delete cap;
+    return CAP_OK;
+}
+
+uint64_t capsule_digest_tokens(const int32_t* ids, uint64_t n) {
+    uint64_t h = 0xcbf29ce484222325ULL;
+    if (!ids) return h;
+    for (uint64_t i = 0; i < n; ++i) {
+        const uint32_t u = (uint32_t)ids[i];
+        for (int byte = 0; byte < 4; ++byte) {
+            h ^= (u >> (8 * byte)) & 0xFFu;
+            h *= 0x100000001b3ULL;
+        }
+    }
+    return h;
+}
+
+int linattn_chunked_prefill(const linattn_args* a, void* stream) {
+    if (!a) return CAP_E_INVAL;
+    if (a->T < 0 || a->H < 1 || a->dk < 1 || a->dv < 1 || a->chunk < 1) return CAP_E_INVAL;
+    if (a->in_dtype != CAP_DTYPE_BF16 && a->in_dtype != CAP_DTYPE_F32) return CAP_E_INVAL;
+    if (a->chunk != 64 || (a->dk != 64 && a->dk != 128) || (a->dv % 16) != 0) return CAP_E_UNSUPPORTED;
+    if (a->in_dtype == CAP_DTYPE_F32 && a->dk != 64) return CAP_E_UNSUPPORTED;
+    if ((int64_t)a->H * (a->dv / 16) > 0x7fffffff) return CAP_E_UNSUPPORTED;
+    if (a->T > 0 && (!a->q || !a->k || !a->v || !a->g || !a->o)) return CAP_E_INVAL;
+    const uint64_t ptrs[] = {(uint64_t)(uintptr_t)a->q, (uint64_t)(uintptr_t)a->k, (uint64_t)(uintptr_t)a->v,
+                             (uint64_t)(uintptr_t)a->g, (uint64_t)(uintptr_t)a->state_in,
+                             (uint64_t)(uintptr_t)a->o, (uint64_t)(uintptr_t)a->chunk_states,
+                             (uint64_t)(uintptr_t)a->final_state};
+    for (uint64_t p : ptrs)
+        if (!aligned16(p)) return CAP_E_ALIGN;
+    // outputs must not overlap inputs (final_state may alias state_in)
+    const uint64_t T = (uint64_t)a->T, H = (uint64_t)a->H, dk = (uint64_t)a->dk, dv = (uint64_t)a->dv;
+    const uint64_t es = a->in_dtype == CAP_DTYPE_F32 ? 4 : 2;
+    const uint64_t nck = (T + 63) / 64;
+    struct R { uint64_t p, n; };
+    const R in[] = {{ptrs[0], T * H * dk * es}, {ptrs[1], T * H * dk * es}, {ptrs[2], T * H * dv * es},
+                    {ptrs[3], T * H * 4}, {ptrs[4], H * dk * dv * 4}};
+    const R outr[] = {{ptrs[5], T * H * dv * 4}, {ptrs[6], nck * H * dk * dv * 4}, {ptrs[7], H * dk * dv * 4}};
+    for (int i = 0; i < 3; ++i) {
+        if (!outr[i].p || !outr[i].n) continue;
+        for (int j = 0; j < 5; ++j) {
+            if (!in[j].p || !in[j].n) continue;
+            if (i == 2 && j == 4 && outr[i].p == in[j].p) continue;  // in-place state update
+            if (overlaps(outr[i].p, outr[i].p + outr[i].n, in[j].p, in[j].p + in[j].n)) return CAP_E_INVAL;
+        }
+        for (int j = 0; j < i; ++j) {
+            if (!outr[j].p || !outr[j].n) continue;
+            if (overlaps(outr[i].p, outr[i].p + outr[i].n, outr[j].p, outr[j].p + outr[j].n)) return CAP_E_INVAL;
+        }
+    }
+    cap::ScanParams p{};
+    p.q = a->q; p.k = a->k; p.v = a->v; p.g = a->g;
+    p.state_in = a->state_in; p.o = a->o; p.chunk_states = a->chunk_states; p.final_state = a->final_state;
+    p.T = a->T; p.H = a->H; p.dk = a->dk; p.dv = a->dv;
+    p.in_f32 = a->in_dtype == CAP_DTYPE_F32 ? 1 : 0;
+    p.scale = a->scale;
+    if (a->T == 0 && !a->final_state) return CAP_OK;
+    return launch_status(cap::launch_linattn_scan(p, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

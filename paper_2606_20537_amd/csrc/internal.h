@@ -1,0 +1,69 @@
+// Internal interface between the host ABI (capsule_host.cpp) and the HIP
+// kernels (capsule_copy.hip, linattn_scan.hip).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+namespace cap {
+
+// One entry of a live set's static device segment table.  For buffer i of a
+// set, with the boundary P' chosen per call:
+//   capsule byte offset of buffer i = a + P' * b
+// where a sums the bytes of the fixed buffers before i and b sums the
+// row_bytes of the positional buffers before i.  Entry n (one past the last
+// buffer) carries the totals, so the capsule size is a[n] + P' * b[n] and
+// buffer i occupies [a[i] + P' b[i], a[i+1] + P' b[i+1]).  All values are
+// multiples of 16 bytes.
+struct SegEntry {
+    uint64_t ptr;  // live device address of buffer i (0 in entry n)
+    uint64_t a;
+    uint64_t b;
+};
+
+constexpr int kMaxRep = 64;   // sources (gather environments) per launch
+constexpr int kMaxDst = 16;   // destinations per source (fork)
+constexpr int kMaxPtrLds = 2048;  // live pointers one copy block holds in LDS
+
+enum CopyMode : int { kLiveToArena = 0, kArenaToLive = 1 };
+
+// Per-launch arguments of the copy kernel, passed by value.
+//   kLiveToArena : rep 0 copies set `tabs[0]` -> arena_out.
+//   kArenaToLive : rep r copies arena_in[r] -> n_dst destination sets
+//                  tabs[r * n_dst + d] (fork: one rep, n_dst sets;
+//                  gather: n_rep reps, one set each).
+struct CopyParams {
+    const SegEntry* layout;            // any table of the call (shared a, b)
+    const SegEntry* tabs[kMaxRep];
+    const uint8_t*  arena_in[kMaxRep];
+    uint8_t*        arena_out;
+    uint64_t        P;                 // aligned boundary
+    uint64_t        nvec;              // capsule bytes / 16
+    uint32_t        n_seg;
+    uint32_t        n_dst;
+    uint32_t        n_rep;
+    int32_t         mode;
+};
+
+// Launch the descriptor-driven copy.  Returns hipSuccess or the launch error.
+hipError_t launch_copy(const CopyParams& p, int num_cus, hipStream_t stream);
+
+// Scan arguments after host validation (sizes as 64-bit, pointers raw).
+struct ScanParams {
+    const void*  q;
+    const void*  k;
+    const void*  v;
+    const float* g;
+    const float* state_in;
+    float*       o;
+    float*       chunk_states;
+    float*       final_state;
+    int64_t      T;
+    int32_t      H, dk, dv;
+    int32_t      in_f32;   // 1: q/k/v are fp32, 0: bf16
+    float        scale;
+};
+
+hipError_t launch_linattn_scan(const ScanParams& p, hipStream_t stream);
+
+}  // namespace cap

@@ -1,0 +1,325 @@
+"""Benchmark of the capsule + chunked-scan hot path on one MI355X.
+
+Workload (default): the 48-layer hybrid stack -- 36 gated linear-attention
+layers (32 heads, dk = dv = 128) and 12 full-attention layers (4 KV heads,
+d = 256, K and V bf16), prefix 16384, chunk 64, conv tails 4 x 4096 bf16 per
+linear layer.  One step is one pass of the whole hot path:
+
+  1. cold chunked prefill of the 36 linear layers, writing o and the state at
+     every chunk boundary (the scan's full output)            -> scan tokens/s
+  2. the same prefill writing only o and the final state (the cold-TTFT path)
+  3. snapshot of the live set at P = 16384 (881,983,488 B)
+  4. restore of that capsule into the live set                -> restore GB/s
+  5. fork of the capsule into 4 sibling sessions (read once, write 4x)
+  6. one continuation token through the 36 linear layers from the restored
+     state (T = 1 prefill calls)
+
+Every phase is bracketed by HIP events recorded on the stream the kernels run
+on.  restore/cold TTFT = (phase 2 + phase 6) / (phase 4 + phase 6).
+
+The JSON line's `value` is the capsule restore bandwidth (GB/s, bytes read +
+written); the scan and TTFT figures ride along as extra keys.  `roofline`
+covers the dominant kernel (the scan, phase 1) and `roofline_copy` the restore.
+Inputs are synthetic (synth module, fixed seeds); 4 distinct layers of q/k/v/g
+are generated on the host and copied into the 36 layers' own device buffers.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, GB/s
+MFMA_BF16_PEAK_TFS = 2500.0  # MI355X dense bf16 MFMA, TFLOP/s
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="hybrid48")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--distinct-layers", type=int, default=4)
+    return ap.parse_args()
+
+
+def scan_bytes(T, H, dk, dv, chunk_states):
+    """Algorithmic HBM bytes of one prefill launch (bf16 q,k,v; fp32 g, o,
+    states; zero entering state)."""
+    n_chunks = (T + 63) // 64
+    b = T * H * (2 * (2 * dk + dv) + 4 + 4 * dv) + H * dk * dv * 4
+    if chunk_states:
+        b += n_chunks * H * dk * dv * 4
+    return b
+
+
+def scan_useful_flops(T, H, dk, dv, C=64):
+    """Causal useful flops: per chunk of L tokens, QK^T over the causal half,
+    P V, Q S and the state fold."""
+    full, tail = divmod(T, C)
+    def chunk(L):
+        return 2 * (L * (L + 1) // 2) * (dk + dv) + 2 * 2 * L * dk * dv
+    return H * (full * chunk(C) + (chunk(tail) if tail else 0))
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(w, capsule_layout):
+    """The oracle, as it stands, on the host: single-threaded C (fp64 scan,
+    memcpy capsule).  Bounded sample, scaled to the metric's units."""
+    import numpy as np
+
+    import oracle
+    import synth
+
+    orc = oracle.get()
+    # capsule restore: host memcpy of the whole capsule, median of 5
+    rb, rt, kd = capsule_layout
+    Pa = w.prefix
+    bufs = [np.zeros(r * n, np.uint8) for r, n in zip(rb, rt)]
+    nbytes = orc.capsule_bytes(rb, rt, kd, Pa)
+    arena = np.ones(nbytes, np.uint8)
+    orc.restore(arena, bufs, rb, rt, kd, Pa)  # touch pages
+    ts = []
+    for _ in range(5):
+        t0 = time.perf_counter()
+        orc.restore(arena, bufs, rb, rt, kd, Pa)
+        ts.append(time.perf_counter() - t0)
+    t_restore = float(np.median(ts))
+    restore_gbs = 2 * nbytes / t_restore / 1e9
+    # scan: sequential recurrence on 1 layer x 2 heads x the full prefix
+    H_s = 2
+    inp = synth.linattn_inputs(w.seed, 0, w.prefix, H_s, w.dk, w.dv, "bf16")
+    t0 = time.perf_counter()
+    orc.sequential(inp["q"], inp["k"], inp["v"], inp["g"])
+    t_scan = time.perf_counter() - t0
+    stack_tok_s = w.prefix / (t_scan * w.n_linear * (w.heads / H_s))
+    return {
+        "cpu_baseline": {
+            "value": round(restore_gbs, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": "oracle capsule restore (host memcpy, single thread) of the full %d-byte capsule, "
+                      "median of 5; host %s, %d cores available" % (nbytes, cpu_model(), len(os.sched_getaffinity(0))),
+        },
+        "cpu_baseline_scan": {
+            "value": round(stack_tok_s, 3), "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": "oracle sequential recurrence (fp64, single thread) on 1 layer x %d of %d heads x %d tokens "
+                      "in %.2f s, extrapolated x%d layers x%d head groups" % (
+                          H_s, w.heads, w.prefix, t_scan, w.n_linear, w.heads // H_s),
+        },
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the capsule + scan hot path runs on a single MI355X; "
+              "run it with --gpus 1 (the multi-GPU sharding is a design note, not a measured path).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2606_20537_amd as cap
+    import synth
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    w = synth.get_config(args.workload)
+    T, H, dk, dv, P = w.prefix, w.heads, w.dk, w.dv, w.prefix
+    n_lin, n_full = w.n_linear, w.n_full
+    n_chunks = (T + 63) // 64
+    stream = torch.cuda.Stream(device=dev)  # default priority
+
+    # ---- inputs: distinct host-generated layers replicated into per-layer buffers
+    t_setup = time.perf_counter()
+    nd = max(1, min(args.distinct_layers, n_lin))
+    src = []
+    for l in range(nd):
+        inp = synth.linattn_inputs(w.seed, l, T, H, dk, dv, "bf16")
+        src.append({n: torch.from_numpy(inp[n + "_dev"].view(np.int16)).view(torch.bfloat16).to(dev)
+                    for n in ("q", "k", "v")})
+        src[-1]["g"] = torch.from_numpy(inp["g"]).to(dev)
+        del inp
+    layers = []
+    for l in range(n_lin):
+        s = src[l % nd]
+        layers.append({
+            "q": s["q"].clone(), "k": s["k"].clone(), "v": s["v"].clone(), "g": s["g"].clone(),
+            "o": torch.empty((T, H, dv), dtype=torch.float32, device=dev),
+            "cs": torch.empty((n_chunks, H, dk, dv), dtype=torch.float32, device=dev),
+            "state": torch.empty((H, dk, dv), dtype=torch.float32, device=dev),
+            "conv": torch.empty(w.conv_width * w.conv_channels * 2, dtype=torch.uint8, device=dev),
+            "q1": s["q"][T - 1:T].clone(), "k1": s["k"][T - 1:T].clone(), "v1": s["v"][T - 1:T].clone(),
+            "g1": s["g"][T - 1:T].clone(), "o1": torch.empty((1, H, dv), dtype=torch.float32, device=dev),
+        })
+        layers[-1]["conv"].copy_(torch.from_numpy(synth.fill_normal_bytes(w.seed, l, "conv", layers[-1]["conv"].numel())))
+    del src
+    kv = []
+    for l in range(n_full):
+        for name in ("k", "v"):
+            t = torch.empty(w.t_max * w.kv_row_bytes, dtype=torch.uint8, device=dev)
+            t.view(torch.bfloat16).normal_(generator=torch.Generator(device=dev).manual_seed(w.seed + 2 * l + (name == "v")))
+            kv.append(("kv%d.%s" % (l, name), t))
+
+    def live_bufs(lays, kvs):
+        bufs, li, ki = [], 0, 0
+        for layer in range(n_lin + n_full):  # 3 linear layers, then 1 full-attention layer
+            if layer % 4 == 3 and ki < len(kvs):
+                for _ in range(2):
+                    name, t = kvs[ki]
+                    bufs.append((name, t, w.kv_row_bytes, w.t_max, cap.CAP_KIND_POSITIONAL))
+                    ki += 1
+            else:
+                L = lays[li]
+                bufs.append(("lin%d.state" % li, L["state"], H * dk * dv * 4, 1, cap.CAP_KIND_FIXED))
+                bufs.append(("lin%d.conv" % li, L["conv"], L["conv"].numel(), 1, cap.CAP_KIND_FIXED))
+                li += 1
+        assert li == n_lin and ki == len(kvs)
+        return bufs
+
+    bufs = live_bufs(layers, kv)
+    deploy = 0x48_3A_36_2B_12
+    live = cap.cap_set_create(bufs, w.chunk, deploy)
+    cap_bytes = cap.capsule_bytes(live, P)
+    arena = torch.empty(cap_bytes, dtype=torch.uint8, device=dev)
+    n_fork = dict(w.extra).get("fork", 4)
+    fork_sets, fork_keep = [], []
+    for f in range(n_fork):
+        fl = [{"state": torch.empty_like(L["state"]), "conv": torch.empty_like(L["conv"])} for L in layers]
+        fk = [(n, torch.empty_like(t)) for n, t in kv]
+        fork_keep.append((fl, fk))
+        fork_sets.append(cap.cap_set_create(live_bufs(fl, fk), w.chunk, deploy))
+    flush = torch.empty(512 * 1024 * 1024, dtype=torch.uint8, device=dev)  # > MALL
+    digest = cap.capsule_digest_tokens(synth.token_ids(w.seed, P))
+    torch.cuda.synchronize()
+    t_setup = time.perf_counter() - t_setup
+
+    phases = ["scan_cs", "scan_final", "snapshot", "restore", "fork", "continue"]
+
+    def step(record):
+        ev = {k: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for k in phases}
+        caps = []
+        with torch.cuda.stream(stream):
+            ev["scan_cs"][0].record(stream)
+            for L in layers:
+                cap.linattn_chunked_prefill(L["q"], L["k"], L["v"], L["g"], L["o"], chunk_states=L["cs"],
+                                            final_state=L["state"], stream=stream)
+            ev["scan_cs"][1].record(stream)
+            ev["scan_final"][0].record(stream)
+            for L in layers:
+                cap.linattn_chunked_prefill(L["q"], L["k"], L["v"], L["g"], L["o"], final_state=L["state"],
+                                            stream=stream)
+            ev["scan_final"][1].record(stream)
+            cap.cap_set_set_position(live, P)
+            flush.fill_(1)
+            ev["snapshot"][0].record(stream)
+            c = cap.capsule_snapshot(live, P, digest, arena, stream=stream)
+            ev["snapshot"][1].record(stream)
+            caps.append(c)
+            flush.fill_(2)
+            ev["restore"][0].record(stream)
+            cap.capsule_restore(c, live, digest, stream=stream)
+            ev["restore"][1].record(stream)
+            flush.fill_(3)
+            ev["fork"][0].record(stream)
+            cap.capsule_fork(c, fork_sets, digest, stream=stream)
+            ev["fork"][1].record(stream)
+            ev["continue"][0].record(stream)
+            for L in layers:
+                cap.linattn_chunked_prefill(L["q1"], L["k1"], L["v1"], L["g1"], L["o1"], state_in=L["state"],
+                                            final_state=L["state"], stream=stream)
+            ev["continue"][1].record(stream)
+        return ev, caps
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+
+    # ---- timed region: K steps between barriers (one process: synchronize)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    recs = [step(True) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    ms = {k: float(np.mean([r[0][k][0].elapsed_time(r[0][k][1]) for r in recs])) for k in phases}
+    ms_per_step = wall * 1e3 / args.steps
+
+    # post-run spot check: every fork branch holds the capsule's bytes (the
+    # set starts with lin0.state; KV is not touched by the continuation)
+    nst = H * dk * dv * 4
+    for fl, fk in fork_keep:
+        assert torch.equal(fl[0]["state"].view(torch.uint8).flatten(), arena[:nst])
+        assert torch.equal(fk[-1][1][: P * w.kv_row_bytes], kv[-1][1][: P * w.kv_row_bytes])
+
+    scan_b = scan_bytes(T, H, dk, dv, True)
+    scan_b_final = scan_bytes(T, H, dk, dv, False)
+    flops = scan_useful_flops(T, H, dk, dv)
+    scan_launch_ms = ms["scan_cs"] / n_lin
+    scan_gbs = scan_b / (scan_launch_ms * 1e-3) / 1e9
+    restore_gbs = 2 * cap_bytes / (ms["restore"] * 1e-3) / 1e9
+    cold_ttft = ms["scan_final"] + ms["continue"]
+    caps_ttft = ms["restore"] + ms["continue"]
+
+    out = {
+        "metric": "capsule restore GB/s (% HBM peak); scan tokens/s (% MFMA); restore/cold TTFT",
+        "value": round(restore_gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u8 capsule bytes; scan bf16 MFMA inputs, fp32 state",
+        "data": "synthetic (seeded PCG64; %d distinct layers replicated into %d layer buffers)" % (nd, n_lin),
+        "config": {"workload": "hybrid48: %d linear-attn (H=%d, dk=dv=%d) + %d full-attn (4 KV heads, d=256) layers, "
+                               "prefix %d, chunk 64, fork x%d" % (n_lin, H, dk, n_full, T, n_fork),
+                   "capsule_bytes": cap_bytes, "prefix": T, "chunk": 64},
+        "restore_pct_hbm_peak": round(100 * restore_gbs / HBM_PEAK_GBS, 2),
+        "scan_tokens_per_s": round(T / (ms["scan_cs"] * 1e-3), 1),
+        "scan_tokens_per_s_final_only": round(T / (ms["scan_final"] * 1e-3), 1),
+        "scan_pct_mfma_useful": round(100 * flops / (scan_launch_ms * 1e-3) / (MFMA_BF16_PEAK_TFS * 1e12), 3),
+        "ttft_ms": {"cold_scan_only": round(cold_ttft, 4), "capsule": round(caps_ttft, 4),
+                    "restore_over_cold_ratio": round(cold_ttft / caps_ttft, 3)},
+        "phase_ms": {k: round(v, 4) for k, v in ms.items()},
+        "fork_gbs": round((1 + n_fork) * cap_bytes / (ms["fork"] * 1e-3) / 1e9, 2),
+        "snapshot_gbs": round(2 * cap_bytes / (ms["snapshot"] * 1e-3) / 1e9, 2),
+        "roofline": {"kernel": "linattn_scan_kernel<128,bf16> (with chunk states)", "bound": "hbm",
+                     "achieved": round(scan_gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(scan_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "algorithmic_bytes_per_launch": scan_b, "avg_launch_ms": round(scan_launch_ms, 5)},
+        "roofline_copy": {"kernel": "capsule_copy_kernel (restore)", "bound": "hbm",
+                          "achieved": round(restore_gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                          "frac": round(restore_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                          "algorithmic_bytes_per_launch": 2 * cap_bytes, "avg_launch_ms": round(ms["restore"], 5)},
+        "roofline_scan_final_only": {"bound": "hbm", "algorithmic_bytes_per_launch": scan_b_final,
+                                     "achieved": round(scan_b_final / (ms["scan_final"] / n_lin * 1e-3) / 1e9, 2),
+                                     "unit": "GB/s"},
+        "setup_s": round(t_setup, 1),
+    }
+    if not args.no_cpu_baseline:
+        rb = [b[2] for b in bufs]
+        rt = [b[3] for b in bufs]
+        kd = [b[4] for b in bufs]
+        out.update(cpu_baseline(w, (rb, rt, kd)))
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

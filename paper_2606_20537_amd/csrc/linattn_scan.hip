@@ -17,23 +17,28 @@
 //
 // Four waves; wave w owns rows 16w..16w+15 of the chunk for the outputs and
 // DK/64 of the DK/16 row tiles of the state.  Every product runs on
-// v_mfma_f32_16x16x32_bf16 with fp32 accumulation:
-//   A^T = K Q^T          exact bf16 operands (inputs), causal tiles only
-//   O  += P V            P = A * decay mask, split hi + lo in bf16
-//   X   = Q S_j          S_j fp32, split hi + lo in bf16
-//   S   = exp(G_last) S + (K * w)^T V   K * w split hi + lo in bf16
+// v_mfma_f32_16x16x32_bf16 with fp32 accumulation, written transposed so that
+// each lane ends with four consecutive value columns (16-byte stores):
+//   A^T = K Q^T              exact bf16 operands (inputs)
+//   O^T = V^T P^T            P = A * causal decay mask, split hi + lo in bf16
+//   X^T = S_j^T Q^T          S_j fp32, split hi + lo in bf16
+//   S^T = exp(G_last) S^T + (V w)^T K     w_m = exp(G_last - G_m) scales the
+//                            16-wide V slice (not the dk-wide K), V w split
+//                            hi + lo, K exact
 // The hi/lo split keeps fp32-derived operands to ~2^-17 relative error, far
-// inside the 2e-3 parity bar, while inputs stay exact.  fp32 inputs (the tiny
-// workload) are split hi + lo on load and use three products per term.
+// inside the 2e-3 parity bar, while inputs stay exact.  fp32 inputs are split
+// hi + lo on load and use three products per term.
 //
-// Operand placement uses the fact that the contraction index may be permuted
-// freely as long as both operands agree: the accumulator of K Q^T already
-// holds, per lane, the P entries that P V needs as its A operand, and the
-// state accumulator holds what Q S needs as its B operand once written to LDS
-// as S^T.  K and V are staged in LDS (K row-major and transposed, V
-// transposed); Q is read straight into registers.  Loads of chunk j+1 are
-// issued before chunk j's math and written to the other LDS stage after it,
-// with one barrier per chunk.
+// LDS holds every tile row-major (K, V, V w and the published S), written with
+// 8- and 16-byte stores.  Operands whose contraction index runs along the rows
+// (V^T, (V w)^T, S^T as A operands; K as the fold's B operand) are read with
+// gfx950's transposing LDS load ds_read_b64_tr_b16: inside a 16-lane group,
+// lane L addresses row k0 + L/4, columns 4(L%4)..+3, and lane n receives
+// column n of rows k0..k0+3.  The contraction index may be permuted freely as
+// long as both operands agree, which lets the accumulator of K Q^T serve
+// directly as the B operand of V^T P^T.  Loads run two chunks ahead in
+// registers and land in the other LDS stage after the current chunk's math;
+// the one barrier per chunk orders LDS only and never waits for global stores.
 #include <hip/hip_runtime.h>
 
 #include "internal.h"
@@ -43,29 +48,51 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int CH = 64;        // chunk length
 constexpr int DVS = 16;       // value columns per workgroup
 constexpr int NT = 256;       // threads per workgroup (4 waves)
-constexpr int MP = CH + 8;    // pitch (elements) of the transposed [x][m] tiles
+constexpr int VP = DVS + 8;   // pitch (elements) of the [m][j] and [d][j] tiles
 
 __device__ inline f32x4 mma(const bf16x8& a, const bf16x8& b, const f32x4& c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
+// Transposing LDS read of a row-major tile with `pitch` elements per row:
+// lane n of each 16-lane group gets tile[k0 + 0..3][n0 + n].
+__device__ inline bf16x4 tr4(const __bf16* tile, int pitch, int k0, int n0, int li) {
+    const __bf16* p = tile + (k0 + (li >> 2)) * pitch + n0 + 4 * (li & 3);
+    const i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)p);
+    return __builtin_bit_cast(bf16x4, v);
+}
+
+__device__ inline bf16x8 cat(const bf16x4& a, const bf16x4& b) {
+    return bf16x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+}
+
+// hi + lo split of fp32 values into bf16 (round to nearest even both times).
+__device__ inline void split8(const float* f, bf16x8& hi, bf16x8& lo) {
+    #pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const __bf16 h = (__bf16)f[e];
+        hi[e] = h;
+        lo[e] = (__bf16)(f[e] - (float)h);
+    }
+}
+
 template <int DK, bool F32>
 struct Smem {
-    static constexpr int KP = DK + 8;      // row pitch of K and S^T (elements)
-    static constexpr int NL = F32 ? 2 : 1; // bf16 planes: hi (and lo)
-    __bf16 k[2][NL][CH * KP];    // K  [m][d]
-    __bf16 kt[2][NL][DK * MP];   // K^T [d][m]
-    __bf16 vt[2][NL][DVS * MP];  // V^T [j][m] of this slice
+    static constexpr int KP = DK + 8;      // row pitch of K (elements)
+    static constexpr int NL = F32 ? 2 : 1; // bf16 planes of the inputs: hi (and lo)
+    __bf16 k[2][NL][CH * KP];    // K     [m][d]
+    __bf16 v[2][NL][CH * VP];    // V     [m][j] (this slice)
+    __bf16 vw[2][2][CH * VP];    // V w   [m][j], hi and lo planes
     float G[2][CH];              // inclusive cumulative log-decay
     float eG[2][CH];             // exp(G_i)
-    float wL[2][CH];             // exp(G_last - G_m)
-    __bf16 st[2][2][DVS * KP];   // S^T [j][d], hi and lo planes
+    __bf16 s[2][2][DK * VP];     // S_j   [d][j], hi and lo planes
 };
 
 // 8 consecutive input elements of one row (16 B of bf16 or 32 B of fp32).
@@ -86,32 +113,49 @@ __device__ inline void load_piece(Piece<F32>& p, const void* base, int64_t elem,
     }
 }
 
-// Split a piece into bf16 hi (and lo, for fp32 inputs) vectors.
 template <bool F32>
-__device__ inline void split_piece(const Piece<F32>& p, bf16x8& hi, bf16x8& lo) {
+__device__ inline void piece_f32(const Piece<F32>& p, float* f) {
     if (F32) {
         const f32x4 a = __builtin_bit_cast(f32x4, p.x[0]);
         const f32x4 b = __builtin_bit_cast(f32x4, p.x[F32 ? 1 : 0]);
-        float f[8] = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
         #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const __bf16 h = (__bf16)f[e];
-            hi[e] = h;
-            lo[e] = (__bf16)(f[e] - (float)h);
-        }
+        for (int e = 0; e < 4; ++e) { f[e] = a[e]; f[4 + e] = b[e]; }
+    } else {
+        const bf16x8 h = __builtin_bit_cast(bf16x8, p.x[0]);
+        #pragma unroll
+        for (int e = 0; e < 8; ++e) f[e] = (float)h[e];
+    }
+}
+
+// A piece as bf16 hi (and lo, for fp32 inputs).
+template <bool F32>
+__device__ inline void split_piece(const Piece<F32>& p, bf16x8& hi, bf16x8& lo) {
+    if (F32) {
+        float f[8];
+        piece_f32<F32>(p, f);
+        split8(f, hi, lo);
     } else {
         hi = __builtin_bit_cast(bf16x8, p.x[0]);
         lo = bf16x8{};
     }
 }
 
-__device__ inline void split8(const float* f, bf16x8& hi, bf16x8& lo) {
-    #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-        const __bf16 h = (__bf16)f[e];
-        hi[e] = h;
-        lo[e] = (__bf16)(f[e] - (float)h);
-    }
+// Register staging of one chunk's global loads.
+template <bool F32, int PK, int NKK>
+struct Stage {
+    Piece<F32> kp[PK];
+    Piece<F32> vp;
+    Piece<F32> qp[NKK];
+    float g;
+};
+
+// Workgroup barrier for LDS traffic only.  Global stores of o and the states
+// are never read back inside the kernel, so the barrier does not wait for
+// them (a plain __syncthreads() would drain every outstanding global access).
+__device__ inline void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
 template <int DK, bool F32>
@@ -121,11 +165,11 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
     constexpr int NL = S_::NL;
     constexpr int NKK = DK / 32;           // k-steps of 32 over dk
     constexpr int PK = (CH * DK / 8) / NT; // K pieces per thread per chunk
-    constexpr int NDW = DK / 64;           // state row tiles per wave
+    constexpr int NDW = DK / 64;           // state tiles (16 rows of d) per wave
     __shared__ S_ sm;
 
     const int tid = threadIdx.x;
-    const int w = tid >> 6;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index, uniform
     const int lane = tid & 63;
     const int li = lane & 15;
     const int grp = lane >> 4;
@@ -143,25 +187,21 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
     const int64_t T = p.T;
     const int64_t n_chunks = (T + CH - 1) / CH;
 
-    // ---- state S[:, j0:j0+16] in accumulator layout: tile u covers rows
-    // (w*NDW+u)*16 + 4*grp + r, column j0 + li.
+    // ---- state, as S^T tiles in accumulator layout: lane (li, grp) of tile u
+    // holds S[d][j0 + 4 grp + r], r = 0..3, with d = (w*NDW + u)*16 + li.
     f32x4 S[NDW];
     #pragma unroll
     for (int u = 0; u < NDW; ++u) {
-        #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int d = (w * NDW + u) * 16 + 4 * grp + r;
-            S[u][r] = p.state_in ? p.state_in[((int64_t)h * DK + d) * dv + j0 + li] : 0.0f;
-        }
+        const int d = (w * NDW + u) * 16 + li;
+        S[u] = p.state_in ? *reinterpret_cast<const f32x4*>(p.state_in + ((int64_t)h * DK + d) * dv + j0 + 4 * grp)
+                          : f32x4{0.f, 0.f, 0.f, 0.f};
     }
 
-    // ---- register staging of one chunk
-    Piece<F32> kp[PK];
-    Piece<F32> vp;
-    Piece<F32> qp[NKK];
-    float gval = 0.0f;
+    using St = Stage<F32, PK, NKK>;
+    St R0, R1;
+    bf16x8 qh[NKK], ql[NKK];
 
-    auto load_chunk = [&](int64_t c) {
+    auto load_chunk = [&](St& R, int64_t c) {
         const int64_t t0 = c * CH;
         #pragma unroll
         for (int u = 0; u < PK; ++u) {
@@ -169,74 +209,72 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
             const int m = pc / (DK / 8);
             const int d0 = (pc % (DK / 8)) * 8;
             const int64_t t = t0 + m;
-            load_piece<F32>(kp[u], p.k, (t * H + h) * DK + d0, t < T);
+            load_piece<F32>(R.kp[u], p.k, (t * H + h) * DK + d0, t < T);
         }
         {
             const int m = (tid >> 1) & 63;
             const int jj = (tid & 1) * 8;
             const int64_t t = t0 + m;
-            load_piece<F32>(vp, p.v, (t * H + h) * dv + j0 + jj, tid < 2 * CH && t < T);
+            load_piece<F32>(R.vp, p.v, (t * H + h) * dv + j0 + jj, tid < 2 * CH && t < T);
         }
         #pragma unroll
         for (int kk = 0; kk < NKK; ++kk) {
             const int64_t t = t0 + 16 * w + li;
-            load_piece<F32>(qp[kk], p.q, (t * H + h) * DK + 32 * kk + 8 * grp, t < T);
+            load_piece<F32>(R.qp[kk], p.q, (t * H + h) * DK + 32 * kk + 8 * grp, t < T);
         }
-        if (w == 0) {
-            const int64_t t = t0 + lane;
-            gval = (t < T) ? p.g[t * H + h] : 0.0f;
-        }
+        const int64_t tg = t0 + lane;
+        R.g = (tg < T) ? p.g[tg * H + h] : 0.0f;
     };
 
-    bf16x8 qh[NKK], ql[NKK];
-
-    auto store_chunk = [&](int b) {
+    auto store_chunk = [&](const St& R, int b) {
         #pragma unroll
         for (int u = 0; u < PK; ++u) {
             const int pc = tid + NT * u;
             const int m = pc / (DK / 8);
             const int d0 = (pc % (DK / 8)) * 8;
             bf16x8 hi, lo;
-            split_piece<F32>(kp[u], hi, lo);
+            split_piece<F32>(R.kp[u], hi, lo);
             *reinterpret_cast<bf16x8*>(&sm.k[b][0][m * KP + d0]) = hi;
             if (F32) *reinterpret_cast<bf16x8*>(&sm.k[b][NL - 1][m * KP + d0]) = lo;
-            #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                sm.kt[b][0][(d0 + e) * MP + m] = hi[e];
-                if (F32) sm.kt[b][NL - 1][(d0 + e) * MP + m] = lo[e];
-            }
         }
-        if (tid < 2 * CH) {
-            const int m = (tid >> 1) & 63;
-            const int jj = (tid & 1) * 8;
-            bf16x8 hi, lo;
-            split_piece<F32>(vp, hi, lo);
-            #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                sm.vt[b][0][(jj + e) * MP + m] = hi[e];
-                if (F32) sm.vt[b][NL - 1][(jj + e) * MP + m] = lo[e];
-            }
+        // every wave scans the chunk's log-gates (lane t holds G_t)
+        float x = R.g;
+        #pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const float y = __shfl_up(x, off, 64);
+            if (lane >= off) x += y;
         }
+        const float glast = __shfl(x, 63, 64);
+        const float wl = __expf(glast - x);  // w_t = exp(G_last - G_t)
         if (w == 0) {
-            float x = gval;
-            #pragma unroll
-            for (int off = 1; off < 64; off <<= 1) {
-                const float y = __shfl_up(x, off, 64);
-                if (lane >= off) x += y;
-            }
-            const float glast = __shfl(x, 63, 64);
             sm.G[b][lane] = x;
             sm.eG[b][lane] = __expf(x);
-            sm.wL[b][lane] = __expf(glast - x);
+        }
+        if (tid < 2 * CH) {  // V rows: raw (hi, lo) and V w (hi, lo)
+            const int m = (tid >> 1) & 63;
+            const int jj = (tid & 1) * 8;
+            const float wm = __shfl(wl, m, 64);
+            float f[8];
+            piece_f32<F32>(R.vp, f);
+            bf16x8 hi, lo;
+            split_piece<F32>(R.vp, hi, lo);
+            *reinterpret_cast<bf16x8*>(&sm.v[b][0][m * VP + jj]) = hi;
+            if (F32) *reinterpret_cast<bf16x8*>(&sm.v[b][NL - 1][m * VP + jj]) = lo;
+            #pragma unroll
+            for (int e = 0; e < 8; ++e) f[e] *= wm;
+            split8(f, hi, lo);
+            *reinterpret_cast<bf16x8*>(&sm.vw[b][0][m * VP + jj]) = hi;
+            *reinterpret_cast<bf16x8*>(&sm.vw[b][1][m * VP + jj]) = lo;
         }
         #pragma unroll
-        for (int kk = 0; kk < NKK; ++kk) split_piece<F32>(qp[kk], qh[kk], ql[kk]);
+        for (int kk = 0; kk < NKK; ++kk) split_piece<F32>(R.qp[kk], qh[kk], ql[kk]);
     };
 
+    // S_j split into bf16 hi/lo planes [d][j] for the next chunk's X^T.
     auto publish_state = [&](int b) {
         #pragma unroll
         for (int u = 0; u < NDW; ++u) {
-            const int d = (w * NDW + u) * 16 + 4 * grp;
+            const int d = (w * NDW + u) * 16 + li;
             bf16x4 hi, lo;
             #pragma unroll
             for (int r = 0; r < 4; ++r) {
@@ -244,120 +282,113 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
                 hi[r] = x;
                 lo[r] = (__bf16)(S[u][r] - (float)x);
             }
-            *reinterpret_cast<bf16x4*>(&sm.st[b][0][li * KP + d]) = hi;
-            *reinterpret_cast<bf16x4*>(&sm.st[b][1][li * KP + d]) = lo;
+            *reinterpret_cast<bf16x4*>(&sm.s[b][0][d * VP + 4 * grp]) = hi;
+            *reinterpret_cast<bf16x4*>(&sm.s[b][1][d * VP + 4 * grp]) = lo;
         }
     };
 
-    if (n_chunks > 0) {
-        load_chunk(0);
-        store_chunk(0);
-        publish_state(0);
-    }
-    __syncthreads();
-
-    for (int64_t c = 0; c < n_chunks; ++c) {
+    auto chunk_body = [&](int64_t c, St& Rfree, const St& Rnext) {
         const int b = (int)(c & 1);
         const int64_t t0 = c * CH;
-        if (c + 1 < n_chunks) load_chunk(c + 1);
+        if (c + 2 < n_chunks) load_chunk(Rfree, c + 2);
 
         if (p.chunk_states) {
-            float* cs = p.chunk_states + ((c * H + h) * DK) * (int64_t)dv + j0 + li;
             #pragma unroll
-            for (int u = 0; u < NDW; ++u)
-                #pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    cs[(int64_t)((w * NDW + u) * 16 + 4 * grp + r) * dv] = S[u][r];
+            for (int u = 0; u < NDW; ++u) {
+                const int d = (w * NDW + u) * 16 + li;
+                *reinterpret_cast<f32x4*>(p.chunk_states + ((c * H + h) * DK + d) * (int64_t)dv + j0 + 4 * grp) = S[u];
+            }
         }
 
-        // ---- A^T = K Q^T for the causal tiles (m-block mb <= w)
+        // ---- A^T = K Q^T, all four m-blocks; lane (li, grp) of tile mb holds
+        // A^T[m = 16 mb + 4 grp + r][i = 16 w + li]
         f32x4 at[4];
         #pragma unroll
         for (int mb = 0; mb < 4; ++mb) {
+            bf16x8 a[NKK], al[NKK];
+            #pragma unroll
+            for (int kk = 0; kk < NKK; ++kk) {
+                const int off = (mb * 16 + li) * KP + 32 * kk + 8 * grp;
+                a[kk] = *reinterpret_cast<const bf16x8*>(&sm.k[b][0][off]);
+                if (F32) al[kk] = *reinterpret_cast<const bf16x8*>(&sm.k[b][NL - 1][off]);
+            }
             at[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
-            if (mb <= w) {
-                #pragma unroll
-                for (int kk = 0; kk < NKK; ++kk) {
-                    const int off = (mb * 16 + li) * KP + 32 * kk + 8 * grp;
-                    const bf16x8 a = *reinterpret_cast<const bf16x8*>(&sm.k[b][0][off]);
-                    at[mb] = mma(a, qh[kk], at[mb]);
-                    if (F32) {
-                        const bf16x8 al = *reinterpret_cast<const bf16x8*>(&sm.k[b][NL - 1][off]);
-                        at[mb] = mma(a, ql[kk], at[mb]);
-                        at[mb] = mma(al, qh[kk], at[mb]);
-                    }
+            #pragma unroll
+            for (int kk = 0; kk < NKK; ++kk) {
+                at[mb] = mma(a[kk], qh[kk], at[mb]);
+                if (F32) {
+                    at[mb] = mma(a[kk], ql[kk], at[mb]);
+                    at[mb] = mma(al[kk], qh[kk], at[mb]);
                 }
             }
         }
-        // ---- decay mask: P[i][m] = A[i][m] exp(G_i - G_m) for m <= i
+        // ---- causal decay mask: P[i][m] = A[i][m] exp(G_i - G_m) for m <= i
+        const int i_row = 16 * w + li;
         {
-            const int i = 16 * w + li;
-            const float Gi = sm.G[b][i];
+            const float Gi = sm.G[b][i_row];
             #pragma unroll
             for (int mb = 0; mb < 4; ++mb) {
-                if (mb <= w) {
-                    #pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const int m = mb * 16 + 4 * grp + r;
-                        at[mb][r] = (m <= i) ? at[mb][r] * __expf(Gi - sm.G[b][m]) : 0.0f;
-                    }
+                const f32x4 Gm = *reinterpret_cast<const f32x4*>(&sm.G[b][mb * 16 + 4 * grp]);
+                #pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int m = mb * 16 + 4 * grp + r;
+                    const float pv = at[mb][r] * __expf(Gi - Gm[r]);
+                    at[mb][r] = (m <= i_row) ? pv : 0.0f;
                 }
             }
         }
-        // ---- O_intra = P V (pairs of m-blocks per MFMA)
+        // ---- O^T = V^T P^T, two m-blocks per MFMA; lane (li, grp) ends with
+        // O[i = 16 w + li][j0 + 4 grp + r]
         f32x4 acc_o = {0.f, 0.f, 0.f, 0.f};
         #pragma unroll
         for (int pr = 0; pr < 2; ++pr) {
-            if (2 * pr <= w) {
-                float f[8];
-                #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    f[r] = at[2 * pr][r];
-                    f[4 + r] = at[2 * pr + 1][r];
-                }
-                bf16x8 ph, pl;
-                split8(f, ph, pl);
-                const int o0 = li * MP + (2 * pr) * 16 + 4 * grp;
-                const int o1 = li * MP + (2 * pr + 1) * 16 + 4 * grp;
-                bf16x8 vh;
-                const bf16x4 va = *reinterpret_cast<const bf16x4*>(&sm.vt[b][0][o0]);
-                const bf16x4 vb = *reinterpret_cast<const bf16x4*>(&sm.vt[b][0][o1]);
-                #pragma unroll
-                for (int e = 0; e < 4; ++e) { vh[e] = va[e]; vh[4 + e] = vb[e]; }
-                acc_o = mma(ph, vh, acc_o);
-                acc_o = mma(pl, vh, acc_o);
-                if (F32) {
-                    bf16x8 vl;
-                    const bf16x4 la = *reinterpret_cast<const bf16x4*>(&sm.vt[b][NL - 1][o0]);
-                    const bf16x4 lb = *reinterpret_cast<const bf16x4*>(&sm.vt[b][NL - 1][o1]);
-                    #pragma unroll
-                    for (int e = 0; e < 4; ++e) { vl[e] = la[e]; vl[4 + e] = lb[e]; }
-                    acc_o = mma(ph, vl, acc_o);
-                }
+            float f[8];
+            #pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                f[r] = at[2 * pr][r];
+                f[4 + r] = at[2 * pr + 1][r];
+            }
+            bf16x8 ph, pl;
+            split8(f, ph, pl);
+            const bf16x8 vh = cat(tr4(sm.v[b][0], VP, (2 * pr) * 16 + 4 * grp, 0, li),
+                                  tr4(sm.v[b][0], VP, (2 * pr + 1) * 16 + 4 * grp, 0, li));
+            acc_o = mma(vh, ph, acc_o);
+            acc_o = mma(vh, pl, acc_o);
+            if (F32) {
+                const bf16x8 vl = cat(tr4(sm.v[b][NL - 1], VP, (2 * pr) * 16 + 4 * grp, 0, li),
+                                      tr4(sm.v[b][NL - 1], VP, (2 * pr + 1) * 16 + 4 * grp, 0, li));
+                acc_o = mma(vl, ph, acc_o);
             }
         }
-        // ---- X = Q S_j (S_j from the published S^T planes)
+        // ---- X^T = S_j^T Q^T from the published S planes
         f32x4 acc_x = {0.f, 0.f, 0.f, 0.f};
-        #pragma unroll
-        for (int kk = 0; kk < NKK; ++kk) {
-            const int off = li * KP + 32 * kk + 8 * grp;
-            const bf16x8 sh = *reinterpret_cast<const bf16x8*>(&sm.st[b][0][off]);
-            const bf16x8 sl = *reinterpret_cast<const bf16x8*>(&sm.st[b][1][off]);
-            acc_x = mma(qh[kk], sh, acc_x);
-            acc_x = mma(qh[kk], sl, acc_x);
-            if (F32) acc_x = mma(ql[kk], sh, acc_x);
-        }
-        // ---- outputs of rows 16w + 4grp + r
-        #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int i = 16 * w + 4 * grp + r;
-            const int64_t t = t0 + i;
-            if (t < T) {
-                const float val = p.scale * (sm.eG[b][i] * acc_x[r] + acc_o[r]);
-                p.o[(t * H + h) * (int64_t)dv + j0 + li] = val;
+        {
+            bf16x8 sh[NKK], sl[NKK];
+            #pragma unroll
+            for (int kk = 0; kk < NKK; ++kk) {
+                const int k0 = 32 * kk + 8 * grp;
+                sh[kk] = cat(tr4(sm.s[b][0], VP, k0, 0, li), tr4(sm.s[b][0], VP, k0 + 4, 0, li));
+                sl[kk] = cat(tr4(sm.s[b][1], VP, k0, 0, li), tr4(sm.s[b][1], VP, k0 + 4, 0, li));
+            }
+            #pragma unroll
+            for (int kk = 0; kk < NKK; ++kk) {
+                acc_x = mma(sh[kk], qh[kk], acc_x);
+                acc_x = mma(sl[kk], qh[kk], acc_x);
+                if (F32) acc_x = mma(sh[kk], ql[kk], acc_x);
             }
         }
-        // ---- state fold: S = exp(G_last) S + (K * wL)^T V
+        // ---- o row i = 16 w + li, columns j0 + 4 grp .. + 3 (one 16-byte store)
+        {
+            const int64_t t = t0 + i_row;
+            if (t < T) {
+                const float eg = sm.eG[b][i_row];
+                f32x4 val;
+                #pragma unroll
+                for (int r = 0; r < 4; ++r) val[r] = p.scale * (eg * acc_x[r] + acc_o[r]);
+                *reinterpret_cast<f32x4*>(p.o + (t * H + h) * (int64_t)dv + j0 + 4 * grp) = val;
+            }
+        }
+        // ---- state fold: S^T = exp(G_last) S^T + (V w)^T K
         {
             const float decay = sm.eG[b][CH - 1];
             #pragma unroll
@@ -368,47 +399,48 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
             #pragma unroll
             for (int mm = 0; mm < 2; ++mm) {
                 const int m0 = 32 * mm + 8 * grp;
-                float wl[8];
-                #pragma unroll
-                for (int e = 0; e < 8; ++e) wl[e] = sm.wL[b][m0 + e];
-                const bf16x8 vh = *reinterpret_cast<const bf16x8*>(&sm.vt[b][0][li * MP + m0]);
-                bf16x8 vl;
-                if (F32) vl = *reinterpret_cast<const bf16x8*>(&sm.vt[b][NL - 1][li * MP + m0]);
+                const bf16x8 wh = cat(tr4(sm.vw[b][0], VP, m0, 0, li), tr4(sm.vw[b][0], VP, m0 + 4, 0, li));
+                const bf16x8 wlo = cat(tr4(sm.vw[b][1], VP, m0, 0, li), tr4(sm.vw[b][1], VP, m0 + 4, 0, li));
                 #pragma unroll
                 for (int u = 0; u < NDW; ++u) {
-                    const int d = (w * NDW + u) * 16 + li;
-                    const bf16x8 kh = *reinterpret_cast<const bf16x8*>(&sm.kt[b][0][d * MP + m0]);
-                    float f[8];
+                    const int n0 = (w * NDW + u) * 16;
+                    const bf16x8 kh = cat(tr4(sm.k[b][0], KP, m0, n0, li), tr4(sm.k[b][0], KP, m0 + 4, n0, li));
+                    S[u] = mma(wh, kh, S[u]);
+                    S[u] = mma(wlo, kh, S[u]);
                     if (F32) {
-                        const bf16x8 kl = *reinterpret_cast<const bf16x8*>(&sm.kt[b][NL - 1][d * MP + m0]);
-                        #pragma unroll
-                        for (int e = 0; e < 8; ++e) f[e] = ((float)kh[e] + (float)kl[e]) * wl[e];
-                    } else {
-                        #pragma unroll
-                        for (int e = 0; e < 8; ++e) f[e] = (float)kh[e] * wl[e];
+                        const bf16x8 kl = cat(tr4(sm.k[b][NL - 1], KP, m0, n0, li),
+                                              tr4(sm.k[b][NL - 1], KP, m0 + 4, n0, li));
+                        S[u] = mma(wh, kl, S[u]);
                     }
-                    bf16x8 ah, al;
-                    split8(f, ah, al);
-                    S[u] = mma(ah, vh, S[u]);
-                    S[u] = mma(al, vh, S[u]);
-                    if (F32) S[u] = mma(ah, vl, S[u]);
                 }
             }
         }
         // ---- hand the new state and the next chunk to the other stage
         publish_state(b ^ 1);
-        if (c + 1 < n_chunks) store_chunk(b ^ 1);
-        __syncthreads();
+        if (c + 1 < n_chunks) store_chunk(Rnext, b ^ 1);
+        lds_barrier();
+    };
+
+    if (n_chunks > 0) {
+        load_chunk(R0, 0);
+        if (n_chunks > 1) load_chunk(R1, 1);
+        store_chunk(R0, 0);
+        publish_state(0);
+    }
+    lds_barrier();
+
+    // two chunks of loads in flight: chunk c + 2 is fetched while c computes
+    for (int64_t c = 0; c < n_chunks; c += 2) {
+        chunk_body(c, R0, R1);
+        if (c + 1 < n_chunks) chunk_body(c + 1, R1, R0);
     }
 
     if (p.final_state) {
         #pragma unroll
-        for (int u = 0; u < NDW; ++u)
-            #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int d = (w * NDW + u) * 16 + 4 * grp + r;
-                p.final_state[((int64_t)h * DK + d) * dv + j0 + li] = S[u][r];
-            }
+        for (int u = 0; u < NDW; ++u) {
+            const int d = (w * NDW + u) * 16 + li;
+            *reinterpret_cast<f32x4*>(p.final_state + ((int64_t)h * DK + d) * dv + j0 + 4 * grp) = S[u];
+        }
     }
 }
 
@@ -422,9 +454,7 @@ hipError_t launch_t(const ScanParams& p, hipStream_t stream) {
 }  // namespace
 
 hipError_t launch_linattn_scan(const ScanParams& p, hipStream_t stream) {
-    // fp32 inputs keep hi and lo planes of every staged tile; at dk = 128 that
-    // exceeds the 160 KiB of LDS, so fp32 inputs are limited to dk = 64.
-    if (p.dk == 128 && !p.in_f32) return launch_t<128, false>(p, stream);
+    if (p.dk == 128) return p.in_f32 ? launch_t<128, true>(p, stream) : launch_t<128, false>(p, stream);
     if (p.dk == 64) return p.in_f32 ? launch_t<64, true>(p, stream) : launch_t<64, false>(p, stream);
     return hipErrorInvalidValue;
 }

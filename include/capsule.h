@@ -204,7 +204,8 @@ CAP_API uint64_t capsule_digest_tokens(const int32_t* ids, uint64_t n);
  *                  ENTERING chunk j (entry 0 = state_in)
  *   final_state  : [H, dk, dv] fp32 or NULL; the state after the last token.
  *                  May be the same pointer as state_in (in-place update).
- * Supported: chunk == 64, dk in {64, 128}, dv a multiple of 16, 1 <= H,
+ * Supported: chunk == 64, dk in {64, 128} (fp32 inputs: dk == 64), dv a
+ * multiple of 16, 1 <= H,
  * 0 <= T; pointers 16-byte aligned; o / chunk_states / final_state must not
  * overlap the inputs (except final_state == state_in).
  * Errors: CAP_E_INVAL (null required pointer, T < 0, H < 1, bad dtype,

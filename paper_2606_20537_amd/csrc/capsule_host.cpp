@@ -429,6 +429,7 @@ int linattn_chunked_prefill(const linattn_args* a, void* stream) {
     if (a->T < 0 || a->H < 1 || a->dk < 1 || a->dv < 1 || a->chunk < 1) return CAP_E_INVAL;
     if (a->in_dtype != CAP_DTYPE_BF16 && a->in_dtype != CAP_DTYPE_F32) return CAP_E_INVAL;
     if (a->chunk != 64 || (a->dk != 64 && a->dk != 128) || (a->dv % 16) != 0) return CAP_E_UNSUPPORTED;
+    if (a->in_dtype == CAP_DTYPE_F32 && a->dk != 64) return CAP_E_UNSUPPORTED;
     if ((int64_t)a->H * (a->dv / 16) > 0x7fffffff) return CAP_E_UNSUPPORTED;
     if (a->T > 0 && (!a->q || !a->k || !a->v || !a->g || !a->o)) return CAP_E_INVAL;
     const uint64_t ptrs[] = {(uint64_t)(uintptr_t)a->q, (uint64_t)(uintptr_t)a->k, (uint64_t)(uintptr_t)a->v,

@@ -15,30 +15,38 @@
 // That is what makes restore-at-an-aligned-boundary-then-continue bitwise
 // equal to one long prefill.
 //
-// Four waves; wave w owns rows 16w..16w+15 of the chunk for the outputs and
-// DK/64 of the DK/16 row tiles of the state.  Every product runs on
-// v_mfma_f32_16x16x32_bf16 with fp32 accumulation, written transposed so that
-// each lane ends with four consecutive value columns (16-byte stores):
-//   A^T = K Q^T              exact bf16 operands (inputs)
-//   O^T = V^T P^T            P = A * causal decay mask, split hi + lo in bf16
-//   X^T = S_j^T Q^T          S_j fp32, split hi + lo in bf16
-//   S^T = exp(G_last) S^T + (V w)^T K     w_m = exp(G_last - G_m) scales the
-//                            16-wide V slice (not the dk-wide K), V w split
-//                            hi + lo, K exact
-// The hi/lo split keeps fp32-derived operands to ~2^-17 relative error, far
-// inside the 2e-3 parity bar, while inputs stay exact.  fp32 inputs are split
-// hi + lo on load and use three products per term.
+// Eight waves, two per SIMD, in two roles that overlap on every SIMD:
+//   output waves 0-3: wave w owns rows 16w..16w+15 of the chunk and computes
+//     A^T = K Q^T (causal tiles), P = A * decay, O^T = V^T P^T,
+//     X^T = S_j^T Q^T and o = scale (exp(G) X + O);
+//   state waves 4-7: stream the chunk two ahead from HBM into registers,
+//     stage it in LDS, write the chunk-boundary states and fold the state
+//     S^T = exp(G_last) S^T + (V w)^T K over their DK/64 tiles of 16 rows.
+// Every product runs on v_mfma_f32_16x16x32_bf16 with fp32 accumulation,
+// written transposed so that each lane ends with four consecutive value
+// columns (16-byte stores).  Inputs are exact bf16 operands; fp32-derived
+// operands (P, S_j, V w with w_m = exp(G_last - G_m)) are split hi + lo in
+// bf16, which keeps them to ~2^-17 relative error, far inside the 2e-3 parity
+// bar.  Scaling the 16-wide V slice by w instead of the dk-wide K keeps K
+// exact and the split small.  fp32 inputs are split hi + lo on load and use
+// three products per term.
 //
-// LDS holds every tile row-major (K, V, V w and the published S), written with
-// 8- and 16-byte stores.  Operands whose contraction index runs along the rows
-// (V^T, (V w)^T, S^T as A operands; K as the fold's B operand) are read with
-// gfx950's transposing LDS load ds_read_b64_tr_b16: inside a 16-lane group,
-// lane L addresses row k0 + L/4, columns 4(L%4)..+3, and lane n receives
-// column n of rows k0..k0+3.  The contraction index may be permuted freely as
-// long as both operands agree, which lets the accumulator of K Q^T serve
-// directly as the B operand of V^T P^T.  Loads run two chunks ahead in
-// registers and land in the other LDS stage after the current chunk's math;
-// the one barrier per chunk orders LDS only and never waits for global stores.
+// Decay: inside the chunk G is non-increasing for g <= 0.  Below the diagonal
+// tile, exp(G_i - G_m) = exp(G_i - G_e) exp(G_e - G_m) with e the last token of
+// m's 16-token block; both factors lie in (0, 1], come from per-chunk tables
+// and never overflow.  The diagonal tile evaluates exp2 directly.
+//
+// LDS holds every tile row-major (K, Q, V, V w and the published S), written
+// with 8- and 16-byte stores.  Operands whose contraction index runs along the
+// rows (V^T, (V w)^T, S^T as A operands; K as the fold's B operand) are read
+// with gfx950's transposing LDS load ds_read_b64_tr_b16: inside a 16-lane
+// group, lane L addresses row k0 + L/4, columns 4(L%4)..+3, and lane n
+// receives column n of rows k0..k0+3.  The contraction index may be permuted
+// freely as long as both operands agree, which lets the accumulator of K Q^T
+// serve directly as the B operand of V^T P^T.  HBM traffic goes through buffer
+// resources: a scalar base per chunk, fixed per-lane offsets, and hardware
+// range checks that read the ragged tail as zeros and drop stores past T.
+// The one barrier per chunk orders LDS only and never waits for global stores.
 #include <hip/hip_runtime.h>
 
 #include "internal.h"
@@ -51,14 +59,24 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
 
 constexpr int CH = 64;        // chunk length
 constexpr int DVS = 16;       // value columns per workgroup
-constexpr int NT = 256;       // threads per workgroup (4 waves)
+constexpr int NT = 512;       // threads per workgroup (8 waves)
+constexpr int NS_T = 256;     // threads of the state role
 constexpr int VP = DVS + 8;   // pitch (elements) of the [m][j] and [d][j] tiles
+constexpr float LOG2E = 1.4426950408889634f;
 
 __device__ inline f32x4 mma(const bf16x8& a, const bf16x8& b, const f32x4& c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// Buffer resource over [base, base + nbytes) (raw, stride 0); accesses past
+// nbytes read zeros / are dropped.
+__device__ inline rsrc_t make_rsrc(const void* base, int64_t nbytes) {
+    const int64_t n = nbytes < 0 ? 0 : (nbytes > 0x7ffffff0 ? 0x7ffffff0 : nbytes);
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, 0x00020000);
 }
 
 // Transposing LDS read of a row-major tile with `pitch` elements per row:
@@ -70,7 +88,30 @@ __device__ inline bf16x4 tr4(const __bf16* tile, int pitch, int k0, int n0, int 
 }
 
 __device__ inline bf16x8 cat(const bf16x4& a, const bf16x4& b) {
-    return bf16x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+    return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave with DPP row shifts and
+// row broadcasts (cross-lane ALU operations, no LDS round trip).  The
+// association order is fixed, so the result is deterministic.
+template <int CTRL, int ROW_MASK, bool BOUND_ZERO>
+__device__ inline float dpp_f(float x) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, ROW_MASK, 0xf,
+                                                                 BOUND_ZERO));
+}
+
+__device__ inline float wave_inclusive_sum(float x) {
+    x += dpp_f<0x111, 0xf, true>(x);   // row_shr:1
+    x += dpp_f<0x112, 0xf, true>(x);   // row_shr:2
+    x += dpp_f<0x114, 0xf, true>(x);   // row_shr:4
+    x += dpp_f<0x118, 0xf, true>(x);   // row_shr:8  -> inclusive within rows of 16
+    x += dpp_f<0x142, 0xa, false>(x);  // row_bcast:15 into rows 1 and 3
+    x += dpp_f<0x143, 0xc, false>(x);  // row_bcast:31 into rows 2 and 3
+    return x;
+}
+
+__device__ inline float lane_value(float x, int l) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), l));
 }
 
 // hi + lo split of fp32 values into bf16 (round to nearest even both times).
@@ -83,16 +124,21 @@ __device__ inline void split8(const float* f, bf16x8& hi, bf16x8& lo) {
     }
 }
 
+// Every member starts on a 16-byte boundary so that 16-byte LDS accesses
+// compile to single ds_read_b128 / ds_write_b128 instructions.
 template <int DK, bool F32>
-struct Smem {
-    static constexpr int KP = DK + 8;      // row pitch of K (elements)
+struct alignas(16) Smem {
+    static constexpr int KP = DK + 8;      // row pitch of K and Q (elements)
     static constexpr int NL = F32 ? 2 : 1; // bf16 planes of the inputs: hi (and lo)
-    __bf16 k[2][NL][CH * KP];    // K     [m][d]
-    __bf16 v[2][NL][CH * VP];    // V     [m][j] (this slice)
-    __bf16 vw[2][2][CH * VP];    // V w   [m][j], hi and lo planes
-    float G[2][CH];              // inclusive cumulative log-decay
-    float eG[2][CH];             // exp(G_i)
-    __bf16 s[2][2][DK * VP];     // S_j   [d][j], hi and lo planes
+    alignas(16) __bf16 k[2][NL][CH * KP];  // K     [m][d]
+    alignas(16) __bf16 q[2][NL][CH * KP];  // Q     [i][d]
+    alignas(16) __bf16 v[2][NL][CH * VP];  // V     [m][j] (this slice)
+    alignas(16) __bf16 vw[2][2][CH * VP];  // V w   [m][j], hi and lo planes
+    alignas(16) __bf16 s[2][2][DK * VP];   // S_j   [d][j], hi and lo planes
+    alignas(16) float G2[2][CH];           // G_t log2(e), G the inclusive log-decay sum
+    alignas(16) float eG[2][CH];           // exp(G_t)
+    alignas(16) float bm[2][CH];           // exp(G_e - G_m), e = last token of m's block
+    alignas(16) float ai[2][CH][4];        // exp(G_i - G_e(M)) for 16-token blocks M below i's
 };
 
 // 8 consecutive input elements of one row (16 B of bf16 or 32 B of fp32).
@@ -102,15 +148,9 @@ struct Piece {
 };
 
 template <bool F32>
-__device__ inline void load_piece(Piece<F32>& p, const void* base, int64_t elem, bool valid) {
-    if (F32) {
-        const u32x4* s = reinterpret_cast<const u32x4*>(static_cast<const float*>(base) + elem);
-        p.x[0] = valid ? s[0] : u32x4{0, 0, 0, 0};
-        p.x[F32 ? 1 : 0] = valid ? s[1] : u32x4{0, 0, 0, 0};
-    } else {
-        const u32x4* s = reinterpret_cast<const u32x4*>(static_cast<const __bf16*>(base) + elem);
-        p.x[0] = valid ? s[0] : u32x4{0, 0, 0, 0};
-    }
+__device__ inline void load_piece(Piece<F32>& p, rsrc_t r, uint32_t off) {
+    p.x[0] = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+    if (F32) p.x[F32 ? 1 : 0] = __builtin_amdgcn_raw_buffer_load_b128(r, off + 16, 0, 0);
 }
 
 template <bool F32>
@@ -140,12 +180,12 @@ __device__ inline void split_piece(const Piece<F32>& p, bf16x8& hi, bf16x8& lo) 
     }
 }
 
-// Register staging of one chunk's global loads.
-template <bool F32, int PK, int NKK>
+// Register staging of one chunk's global loads (state role only).
+template <bool F32, int PK>
 struct Stage {
     Piece<F32> kp[PK];
+    Piece<F32> qp[PK];
     Piece<F32> vp;
-    Piece<F32> qp[NKK];
     float g;
 };
 
@@ -163,16 +203,20 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
     using S_ = Smem<DK, F32>;
     constexpr int KP = S_::KP;
     constexpr int NL = S_::NL;
-    constexpr int NKK = DK / 32;           // k-steps of 32 over dk
-    constexpr int PK = (CH * DK / 8) / NT; // K pieces per thread per chunk
-    constexpr int NDW = DK / 64;           // state tiles (16 rows of d) per wave
+    constexpr int NKK = DK / 32;             // k-steps of 32 over dk
+    constexpr int PK = (CH * DK / 8) / NS_T; // K (and Q) pieces per state thread
+    constexpr int NDW = DK / 64;             // state tiles (16 rows of d) per state wave
+    constexpr int ES = F32 ? 4 : 2;          // input element size
     __shared__ S_ sm;
 
     const int tid = threadIdx.x;
-    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index, uniform
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform
+    const bool state_role = wave >= 4;
+    const int wq = wave & 3;
     const int lane = tid & 63;
     const int li = lane & 15;
     const int grp = lane >> 4;
+    const int st = tid - NS_T;  // state-role thread index (valid when state_role)
 
     // workgroup -> (head, slice); slices of one head share an XCD (and its L2)
     // when the grid allows it (workgroups go round-robin over 8 XCDs).
@@ -186,74 +230,76 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
 
     const int64_t T = p.T;
     const int64_t n_chunks = (T + CH - 1) / CH;
+    const int64_t qk_row = (int64_t)H * DK * ES;  // bytes per token of q / k
+    const int64_t v_row = (int64_t)H * dv * ES;   // bytes per token of v
+    const int64_t o_row = (int64_t)H * dv * 4;    // bytes per token of o
 
-    // ---- state, as S^T tiles in accumulator layout: lane (li, grp) of tile u
-    // holds S[d][j0 + 4 grp + r], r = 0..3, with d = (w*NDW + u)*16 + li.
+    // ---- state (state role), as S^T tiles in accumulator layout: lane
+    // (li, grp) of tile u holds S[d][j0 + 4 grp + r] with d = (wq*NDW + u)*16 + li.
     f32x4 S[NDW];
     #pragma unroll
-    for (int u = 0; u < NDW; ++u) {
-        const int d = (w * NDW + u) * 16 + li;
-        S[u] = p.state_in ? *reinterpret_cast<const f32x4*>(p.state_in + ((int64_t)h * DK + d) * dv + j0 + 4 * grp)
-                          : f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int u = 0; u < NDW; ++u) S[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (state_role && p.state_in) {
+        #pragma unroll
+        for (int u = 0; u < NDW; ++u) {
+            const int d = (wq * NDW + u) * 16 + li;
+            S[u] = *reinterpret_cast<const f32x4*>(p.state_in + ((int64_t)h * DK + d) * dv + j0 + 4 * grp);
+        }
     }
 
-    using St = Stage<F32, PK, NKK>;
-    St R0, R1;
-    bf16x8 qh[NKK], ql[NKK];
+    using St = Stage<F32, PK>;
 
+    // ---------------------------------------------------------- state role
+    // Every global access of the state loop is issued unconditionally (chunks
+    // past the end get an empty buffer range: loads read zeros, stores are
+    // dropped), so the compiler's in-order memory counters stay exact and the
+    // prefetch of chunk c + 2 is never drained while chunk c computes.
     auto load_chunk = [&](St& R, int64_t c) {
         const int64_t t0 = c * CH;
+        const int64_t rows = T - t0;
+        const rsrc_t rk = make_rsrc(static_cast<const char*>(p.k) + t0 * qk_row, rows * qk_row);
+        const rsrc_t rq = make_rsrc(static_cast<const char*>(p.q) + t0 * qk_row, rows * qk_row);
         #pragma unroll
         for (int u = 0; u < PK; ++u) {
-            const int pc = tid + NT * u;
+            const int pc = st + NS_T * u;
             const int m = pc / (DK / 8);
             const int d0 = (pc % (DK / 8)) * 8;
-            const int64_t t = t0 + m;
-            load_piece<F32>(R.kp[u], p.k, (t * H + h) * DK + d0, t < T);
+            const uint32_t off = (uint32_t)(m * qk_row + ((int64_t)h * DK + d0) * ES);
+            load_piece<F32>(R.kp[u], rk, off);
+            load_piece<F32>(R.qp[u], rq, off);
         }
-        {
-            const int m = (tid >> 1) & 63;
-            const int jj = (tid & 1) * 8;
-            const int64_t t = t0 + m;
-            load_piece<F32>(R.vp, p.v, (t * H + h) * dv + j0 + jj, tid < 2 * CH && t < T);
-        }
-        #pragma unroll
-        for (int kk = 0; kk < NKK; ++kk) {
-            const int64_t t = t0 + 16 * w + li;
-            load_piece<F32>(R.qp[kk], p.q, (t * H + h) * DK + 32 * kk + 8 * grp, t < T);
-        }
-        const int64_t tg = t0 + lane;
-        R.g = (tg < T) ? p.g[tg * H + h] : 0.0f;
+        // V slice: 128 pieces for state threads 0..127; threads 128..255 fetch
+        // the same pieces (L2 hits) so that all state waves run one stream
+        const rsrc_t rv = make_rsrc(static_cast<const char*>(p.v) + t0 * v_row, rows * v_row);
+        const int vs = st & 127;
+        load_piece<F32>(R.vp, rv, (uint32_t)((vs >> 1) * v_row + ((int64_t)h * dv + j0 + (vs & 1) * 8) * ES));
+        const rsrc_t rg = make_rsrc(p.g + t0 * H, rows * H * 4);
+        R.g = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rg, (uint32_t)((lane * H + h) * 4), 0, 0));
     };
 
     auto store_chunk = [&](const St& R, int b) {
         #pragma unroll
         for (int u = 0; u < PK; ++u) {
-            const int pc = tid + NT * u;
+            const int pc = st + NS_T * u;
             const int m = pc / (DK / 8);
             const int d0 = (pc % (DK / 8)) * 8;
             bf16x8 hi, lo;
             split_piece<F32>(R.kp[u], hi, lo);
             *reinterpret_cast<bf16x8*>(&sm.k[b][0][m * KP + d0]) = hi;
             if (F32) *reinterpret_cast<bf16x8*>(&sm.k[b][NL - 1][m * KP + d0]) = lo;
+            split_piece<F32>(R.qp[u], hi, lo);
+            *reinterpret_cast<bf16x8*>(&sm.q[b][0][m * KP + d0]) = hi;
+            if (F32) *reinterpret_cast<bf16x8*>(&sm.q[b][NL - 1][m * KP + d0]) = lo;
         }
-        // every wave scans the chunk's log-gates (lane t holds G_t)
-        float x = R.g;
-        #pragma unroll
-        for (int off = 1; off < 64; off <<= 1) {
-            const float y = __shfl_up(x, off, 64);
-            if (lane >= off) x += y;
-        }
-        const float glast = __shfl(x, 63, 64);
+        // every state wave scans the chunk's log-gates: lane t holds G_t
+        const float x = wave_inclusive_sum(R.g);
+        const float glast = lane_value(x, 63);
         const float wl = __expf(glast - x);  // w_t = exp(G_last - G_t)
-        if (w == 0) {
-            sm.G[b][lane] = x;
-            sm.eG[b][lane] = __expf(x);
-        }
-        if (tid < 2 * CH) {  // V rows: raw (hi, lo) and V w (hi, lo)
-            const int m = (tid >> 1) & 63;
-            const int jj = (tid & 1) * 8;
-            const float wm = __shfl(wl, m, 64);
+        const int vs = st & 127;
+        const float wm = __shfl(wl, vs >> 1, 64);
+        if (wave < 6) {  // V rows: raw (hi, lo) and V w (hi, lo)
+            const int m = vs >> 1;
+            const int jj = (vs & 1) * 8;
             float f[8];
             piece_f32<F32>(R.vp, f);
             bf16x8 hi, lo;
@@ -266,15 +312,26 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
             *reinterpret_cast<bf16x8*>(&sm.vw[b][0][m * VP + jj]) = hi;
             *reinterpret_cast<bf16x8*>(&sm.vw[b][1][m * VP + jj]) = lo;
         }
-        #pragma unroll
-        for (int kk = 0; kk < NKK; ++kk) split_piece<F32>(R.qp[kk], qh[kk], ql[kk]);
+        if (wave == 4) {  // decay tables
+            float ge[4];
+            #pragma unroll
+            for (int M = 0; M < 4; ++M) ge[M] = lane_value(x, 16 * M + 15);
+            const int blk = lane >> 4;
+            sm.G2[b][lane] = x * LOG2E;
+            sm.eG[b][lane] = __expf(x);
+            sm.bm[b][lane] = __expf(ge[blk] - x);
+            f32x4 a;
+            #pragma unroll
+            for (int M = 0; M < 4; ++M) a[M] = (M < blk) ? __expf(x - ge[M]) : 0.0f;
+            *reinterpret_cast<f32x4*>(&sm.ai[b][lane][0]) = a;
+        }
     };
 
     // S_j split into bf16 hi/lo planes [d][j] for the next chunk's X^T.
     auto publish_state = [&](int b) {
         #pragma unroll
         for (int u = 0; u < NDW; ++u) {
-            const int d = (w * NDW + u) * 16 + li;
+            const int d = (wq * NDW + u) * 16 + li;
             bf16x4 hi, lo;
             #pragma unroll
             for (int r = 0; r < 4; ++r) {
@@ -287,80 +344,117 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
         }
     };
 
-    auto chunk_body = [&](int64_t c, St& Rfree, const St& Rnext) {
-        const int b = (int)(c & 1);
-        const int64_t t0 = c * CH;
-        if (c + 2 < n_chunks) load_chunk(Rfree, c + 2);
-
-        if (p.chunk_states) {
+    // S^T = exp(G_last) S^T + (V w)^T K over this wave's tiles
+    auto fold = [&](int b) {
+        const float decay = sm.eG[b][CH - 1];
+        #pragma unroll
+        for (int u = 0; u < NDW; ++u) {
+            #pragma unroll
+            for (int r = 0; r < 4; ++r) S[u][r] *= decay;
+        }
+        #pragma unroll
+        for (int mm = 0; mm < 2; ++mm) {
+            const int m0 = 32 * mm + 8 * grp;
+            const bf16x8 wh = cat(tr4(sm.vw[b][0], VP, m0, 0, li), tr4(sm.vw[b][0], VP, m0 + 4, 0, li));
+            const bf16x8 wlo = cat(tr4(sm.vw[b][1], VP, m0, 0, li), tr4(sm.vw[b][1], VP, m0 + 4, 0, li));
             #pragma unroll
             for (int u = 0; u < NDW; ++u) {
-                const int d = (w * NDW + u) * 16 + li;
-                *reinterpret_cast<f32x4*>(p.chunk_states + ((c * H + h) * DK + d) * (int64_t)dv + j0 + 4 * grp) = S[u];
+                const int n0 = (wq * NDW + u) * 16;
+                const bf16x8 kh = cat(tr4(sm.k[b][0], KP, m0, n0, li), tr4(sm.k[b][0], KP, m0 + 4, n0, li));
+                S[u] = mma(wh, kh, S[u]);
+                S[u] = mma(wlo, kh, S[u]);
+                if (F32) {
+                    const bf16x8 kl = cat(tr4(sm.k[b][NL - 1], KP, m0, n0, li),
+                                          tr4(sm.k[b][NL - 1], KP, m0 + 4, n0, li));
+                    S[u] = mma(wh, kl, S[u]);
+                }
             }
         }
+    };
 
-        // ---- A^T = K Q^T, all four m-blocks; lane (li, grp) of tile mb holds
-        // A^T[m = 16 mb + 4 grp + r][i = 16 w + li]
+    // --------------------------------------------------------- output role
+    auto outputs = [&](int b, int64_t c) {
+        const int w = wq;
+        const int i_row = 16 * w + li;
+        bf16x8 qh[NKK], ql[NKK];
+        #pragma unroll
+        for (int kk = 0; kk < NKK; ++kk) {
+            const int off = i_row * KP + 32 * kk + 8 * grp;
+            qh[kk] = *reinterpret_cast<const bf16x8*>(&sm.q[b][0][off]);
+            if (F32) ql[kk] = *reinterpret_cast<const bf16x8*>(&sm.q[b][NL - 1][off]);
+        }
+        // A^T = K Q^T for all four m-blocks (the blocks above the diagonal are
+        // masked to zero below; computing them keeps the path branch-free and
+        // costs no time, since the wave with the most causal blocks sets the
+        // pace); lane (li, grp) of tile mb holds A^T[m = 16 mb + 4 grp + r][i = 16 w + li]
         f32x4 at[4];
         #pragma unroll
         for (int mb = 0; mb < 4; ++mb) {
-            bf16x8 a[NKK], al[NKK];
-            #pragma unroll
-            for (int kk = 0; kk < NKK; ++kk) {
-                const int off = (mb * 16 + li) * KP + 32 * kk + 8 * grp;
-                a[kk] = *reinterpret_cast<const bf16x8*>(&sm.k[b][0][off]);
-                if (F32) al[kk] = *reinterpret_cast<const bf16x8*>(&sm.k[b][NL - 1][off]);
-            }
             at[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
-            #pragma unroll
-            for (int kk = 0; kk < NKK; ++kk) {
-                at[mb] = mma(a[kk], qh[kk], at[mb]);
-                if (F32) {
-                    at[mb] = mma(a[kk], ql[kk], at[mb]);
-                    at[mb] = mma(al[kk], qh[kk], at[mb]);
+            {
+                bf16x8 a[NKK], al[NKK];
+                #pragma unroll
+                for (int kk = 0; kk < NKK; ++kk) {
+                    const int off = (mb * 16 + li) * KP + 32 * kk + 8 * grp;
+                    a[kk] = *reinterpret_cast<const bf16x8*>(&sm.k[b][0][off]);
+                    if (F32) al[kk] = *reinterpret_cast<const bf16x8*>(&sm.k[b][NL - 1][off]);
+                }
+                #pragma unroll
+                for (int kk = 0; kk < NKK; ++kk) {
+                    at[mb] = mma(a[kk], qh[kk], at[mb]);
+                    if (F32) {
+                        at[mb] = mma(a[kk], ql[kk], at[mb]);
+                        at[mb] = mma(al[kk], qh[kk], at[mb]);
+                    }
                 }
             }
         }
-        // ---- causal decay mask: P[i][m] = A[i][m] exp(G_i - G_m) for m <= i
-        const int i_row = 16 * w + li;
+        // decay: factored tables below the diagonal tile, exp2 on it, zero above
         {
-            const float Gi = sm.G[b][i_row];
+            const f32x4 ai = *reinterpret_cast<const f32x4*>(&sm.ai[b][i_row][0]);
+            const float gi = sm.G2[b][i_row];
+            const f32x4 gm = *reinterpret_cast<const f32x4*>(&sm.G2[b][w * 16 + 4 * grp]);
+            f32x4 dg;  // diagonal tile
+            #pragma unroll
+            for (int r = 0; r < 4; ++r)
+                dg[r] = (4 * grp + r <= li) ? __builtin_amdgcn_exp2f(gi - gm[r]) : 0.0f;
             #pragma unroll
             for (int mb = 0; mb < 4; ++mb) {
-                const f32x4 Gm = *reinterpret_cast<const f32x4*>(&sm.G[b][mb * 16 + 4 * grp]);
+                const f32x4 bmv = *reinterpret_cast<const f32x4*>(&sm.bm[b][mb * 16 + 4 * grp]);
                 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    const int m = mb * 16 + 4 * grp + r;
-                    const float pv = at[mb][r] * __expf(Gi - Gm[r]);
-                    at[mb][r] = (m <= i_row) ? pv : 0.0f;
+                    const float below = (at[mb][r] * ai[mb]) * bmv[r];
+                    const float diag = at[mb][r] * dg[r];
+                    at[mb][r] = mb < w ? below : (mb == w ? diag : 0.0f);
                 }
             }
         }
-        // ---- O^T = V^T P^T, two m-blocks per MFMA; lane (li, grp) ends with
+        // O^T = V^T P^T, two m-blocks per MFMA; lane (li, grp) ends with
         // O[i = 16 w + li][j0 + 4 grp + r]
         f32x4 acc_o = {0.f, 0.f, 0.f, 0.f};
         #pragma unroll
         for (int pr = 0; pr < 2; ++pr) {
-            float f[8];
-            #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                f[r] = at[2 * pr][r];
-                f[4 + r] = at[2 * pr + 1][r];
-            }
-            bf16x8 ph, pl;
-            split8(f, ph, pl);
-            const bf16x8 vh = cat(tr4(sm.v[b][0], VP, (2 * pr) * 16 + 4 * grp, 0, li),
-                                  tr4(sm.v[b][0], VP, (2 * pr + 1) * 16 + 4 * grp, 0, li));
-            acc_o = mma(vh, ph, acc_o);
-            acc_o = mma(vh, pl, acc_o);
-            if (F32) {
-                const bf16x8 vl = cat(tr4(sm.v[b][NL - 1], VP, (2 * pr) * 16 + 4 * grp, 0, li),
-                                      tr4(sm.v[b][NL - 1], VP, (2 * pr + 1) * 16 + 4 * grp, 0, li));
-                acc_o = mma(vl, ph, acc_o);
+            {
+                float f[8];
+                #pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    f[r] = at[2 * pr][r];
+                    f[4 + r] = at[2 * pr + 1][r];
+                }
+                bf16x8 ph, pl;
+                split8(f, ph, pl);
+                const bf16x8 vh = cat(tr4(sm.v[b][0], VP, (2 * pr) * 16 + 4 * grp, 0, li),
+                                      tr4(sm.v[b][0], VP, (2 * pr + 1) * 16 + 4 * grp, 0, li));
+                acc_o = mma(vh, ph, acc_o);
+                acc_o = mma(vh, pl, acc_o);
+                if (F32) {
+                    const bf16x8 vl = cat(tr4(sm.v[b][NL - 1], VP, (2 * pr) * 16 + 4 * grp, 0, li),
+                                          tr4(sm.v[b][NL - 1], VP, (2 * pr + 1) * 16 + 4 * grp, 0, li));
+                    acc_o = mma(vl, ph, acc_o);
+                }
             }
         }
-        // ---- X^T = S_j^T Q^T from the published S planes
+        // X^T = S_j^T Q^T from the published S planes
         f32x4 acc_x = {0.f, 0.f, 0.f, 0.f};
         {
             bf16x8 sh[NKK], sl[NKK];
@@ -377,69 +471,69 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
                 if (F32) acc_x = mma(sh[kk], ql[kk], acc_x);
             }
         }
-        // ---- o row i = 16 w + li, columns j0 + 4 grp .. + 3 (one 16-byte store)
+        // o row i = 16 w + li, columns j0 + 4 grp .. + 3: one 16-byte store;
+        // rows past T fall outside the chunk's buffer range and are dropped
         {
-            const int64_t t = t0 + i_row;
-            if (t < T) {
-                const float eg = sm.eG[b][i_row];
-                f32x4 val;
-                #pragma unroll
-                for (int r = 0; r < 4; ++r) val[r] = p.scale * (eg * acc_x[r] + acc_o[r]);
-                *reinterpret_cast<f32x4*>(p.o + (t * H + h) * (int64_t)dv + j0 + 4 * grp) = val;
-            }
-        }
-        // ---- state fold: S^T = exp(G_last) S^T + (V w)^T K
-        {
-            const float decay = sm.eG[b][CH - 1];
+            const int64_t t0 = c * CH;
+            const rsrc_t ro = make_rsrc(reinterpret_cast<const char*>(p.o) + t0 * o_row, (T - t0) * o_row);
+            const float eg = sm.eG[b][i_row];
+            f32x4 val;
             #pragma unroll
-            for (int u = 0; u < NDW; ++u) {
-                #pragma unroll
-                for (int r = 0; r < 4; ++r) S[u][r] *= decay;
-            }
-            #pragma unroll
-            for (int mm = 0; mm < 2; ++mm) {
-                const int m0 = 32 * mm + 8 * grp;
-                const bf16x8 wh = cat(tr4(sm.vw[b][0], VP, m0, 0, li), tr4(sm.vw[b][0], VP, m0 + 4, 0, li));
-                const bf16x8 wlo = cat(tr4(sm.vw[b][1], VP, m0, 0, li), tr4(sm.vw[b][1], VP, m0 + 4, 0, li));
-                #pragma unroll
-                for (int u = 0; u < NDW; ++u) {
-                    const int n0 = (w * NDW + u) * 16;
-                    const bf16x8 kh = cat(tr4(sm.k[b][0], KP, m0, n0, li), tr4(sm.k[b][0], KP, m0 + 4, n0, li));
-                    S[u] = mma(wh, kh, S[u]);
-                    S[u] = mma(wlo, kh, S[u]);
-                    if (F32) {
-                        const bf16x8 kl = cat(tr4(sm.k[b][NL - 1], KP, m0, n0, li),
-                                              tr4(sm.k[b][NL - 1], KP, m0 + 4, n0, li));
-                        S[u] = mma(wh, kl, S[u]);
-                    }
-                }
-            }
+            for (int r = 0; r < 4; ++r) val[r] = p.scale * (eg * acc_x[r] + acc_o[r]);
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, val), ro,
+                                                   (uint32_t)(i_row * o_row + ((int64_t)h * dv + j0 + 4 * grp) * 4), 0, 0);
         }
-        // ---- hand the new state and the next chunk to the other stage
-        publish_state(b ^ 1);
-        if (c + 1 < n_chunks) store_chunk(Rnext, b ^ 1);
-        lds_barrier();
     };
 
-    if (n_chunks > 0) {
+    // One loop per role; both run the same number of barriers.  The loops
+    // advance two chunks per iteration so that the two register stages swap
+    // roles without copies; a chunk index past the end does no visible work.
+    if (state_role) {
+        auto state_step = [&](int64_t c, St& Rfree, const St& Rnext) {
+            const int b = (int)(c & 1);
+            load_chunk(Rfree, c + 2);
+            if (c + 1 < n_chunks) store_chunk(Rnext, b ^ 1);
+            {
+                const bool live = c < n_chunks && p.chunk_states != nullptr;
+                const rsrc_t rc = make_rsrc(p.chunk_states + (live ? c : 0) * (int64_t)H * DK * dv,
+                                            live ? (int64_t)H * DK * dv * 4 : 0);
+                #pragma unroll
+                for (int u = 0; u < NDW; ++u) {
+                    const int d = (wq * NDW + u) * 16 + li;
+                    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, S[u]), rc,
+                                                           (uint32_t)((((int64_t)h * DK + d) * dv + j0 + 4 * grp) * 4), 0, 0);
+                }
+            }
+            if (c < n_chunks) {
+                fold(b);
+                publish_state(b ^ 1);
+            }
+            lds_barrier();
+        };
+        St R0, R1;
         load_chunk(R0, 0);
-        if (n_chunks > 1) load_chunk(R1, 1);
+        load_chunk(R1, 1);
         store_chunk(R0, 0);
         publish_state(0);
-    }
-    lds_barrier();
-
-    // two chunks of loads in flight: chunk c + 2 is fetched while c computes
-    for (int64_t c = 0; c < n_chunks; c += 2) {
-        chunk_body(c, R0, R1);
-        if (c + 1 < n_chunks) chunk_body(c + 1, R1, R0);
-    }
-
-    if (p.final_state) {
-        #pragma unroll
-        for (int u = 0; u < NDW; ++u) {
-            const int d = (w * NDW + u) * 16 + li;
-            *reinterpret_cast<f32x4*>(p.final_state + ((int64_t)h * DK + d) * dv + j0 + 4 * grp) = S[u];
+        lds_barrier();
+        for (int64_t c = 0; c < n_chunks; c += 2) {
+            state_step(c, R0, R1);
+            state_step(c + 1, R1, R0);
+        }
+        if (p.final_state) {
+            #pragma unroll
+            for (int u = 0; u < NDW; ++u) {
+                const int d = (wq * NDW + u) * 16 + li;
+                *reinterpret_cast<f32x4*>(p.final_state + ((int64_t)h * DK + d) * dv + j0 + 4 * grp) = S[u];
+            }
+        }
+    } else {
+        lds_barrier();
+        for (int64_t c = 0; c < n_chunks; c += 2) {
+            outputs(0, c);
+            lds_barrier();
+            outputs(1, c + 1);
+            lds_barrier();
         }
     }
 }
@@ -454,7 +548,9 @@ hipError_t launch_t(const ScanParams& p, hipStream_t stream) {
 }  // namespace
 
 hipError_t launch_linattn_scan(const ScanParams& p, hipStream_t stream) {
-    if (p.dk == 128) return p.in_f32 ? launch_t<128, true>(p, stream) : launch_t<128, false>(p, stream);
+    // fp32 inputs keep hi and lo planes of K, Q and V in LDS; at dk = 128 that
+    // exceeds the 160 KiB of LDS, so fp32 inputs are limited to dk = 64.
+    if (p.dk == 128 && !p.in_f32) return launch_t<128, false>(p, stream);
     if (p.dk == 64) return p.in_f32 ? launch_t<64, true>(p, stream) : launch_t<64, false>(p, stream);
     return hipErrorInvalidValue;
 }

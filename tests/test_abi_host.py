@@ -1,0 +1,157 @@
+"""The C-ABI library on the host, without a GPU: it loads, exports every
+symbol include/capsule.h declares, and its host-side checks return the
+documented status codes before any device call."""
+import ctypes as ct
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2606_20537_amd as cap
+from paper_2606_20537_amd import _native as N
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "capsule.h")
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    return sorted(set(re.findall(r"CAP_API\s+[\w\s\*]+?\b(\w+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared_symbols()
+    assert len(names) >= 15, names
+    lib = ct.CDLL(cap.build.LIB_PATH if hasattr(cap, "build") else N.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), "missing export %s" % n
+    # the binding wraps exactly these entry points
+    assert sorted(s[0] for s in N.SIGNATURES) == names
+
+
+def test_status_strings():
+    for code in (0, -1, -2, -3, -4, -5, -6, -7):
+        assert cap.cap_status_string(code) not in ("", "unknown status")
+    assert cap.cap_status_string(-99) == "unknown status"
+
+
+def test_align_matches_oracle(orc):
+    rng = np.random.default_rng(0)
+    for _ in range(2000):
+        P = int(rng.integers(0, 1 << 40))
+        C = int(rng.integers(1, 4096))
+        assert cap.cap_align_boundary(P, C) == orc.align(P, C)
+    assert cap.cap_align_boundary(123, 0) == 0
+
+
+def test_digest_matches_oracle(orc):
+    rng = np.random.default_rng(1)
+    for n in (0, 1, 7, 2048):
+        ids = rng.integers(-2**31, 2**31 - 1, size=n, dtype=np.int64).astype(np.int32)
+        assert cap.capsule_digest_tokens(ids) == orc.digest_tokens(ids)
+
+
+def _bufs(layout):
+    return [(name, 0, rb, rows, kind) for name, rb, rows, kind in layout]
+
+
+def test_layout_bytes_match_oracle(orc):
+    rng = np.random.default_rng(2)
+    for trial in range(200):
+        n = int(rng.integers(1, 12))
+        layout = []
+        for i in range(n):
+            kind = int(rng.integers(0, 2))
+            layout.append(("b%d" % i, int(rng.integers(1, 64)) * 16, int(rng.integers(1, 300)), kind))
+        chunk = int(rng.integers(1, 100))
+        cap_rows = min([l[2] for l in layout if l[3] == 0], default=10**9)
+        P = int(rng.integers(0, cap_rows + 1))
+        got = cap.capsule_layout_bytes(_bufs(layout), chunk, P)
+        want = orc.capsule_bytes([l[1] for l in layout], [l[2] for l in layout], [l[3] for l in layout],
+                                 orc.align(P, chunk))
+        assert got == want
+
+
+def _status(fn, *a, **k):
+    try:
+        fn(*a, **k)
+    except cap.CapsuleError as e:
+        return e.status
+    return cap.CAP_OK
+
+
+def test_layout_errors():
+    ok = [("k", 64, 100, 0), ("s", 256, 1, 1)]
+    assert _status(cap.capsule_layout_bytes, _bufs(ok), 64, 64) == cap.CAP_OK
+    assert _status(cap.capsule_layout_bytes, _bufs([("k", 64, 100, 7)]), 64, 0) == cap.CAP_E_UNSUPPORTED
+    assert _status(cap.capsule_layout_bytes, _bufs([("k", 24, 100, 0)]), 64, 0) == cap.CAP_E_ALIGN
+    assert _status(cap.capsule_layout_bytes, _bufs([("k", 64, 0, 0)]), 64, 0) == cap.CAP_E_INVAL
+    assert _status(cap.capsule_layout_bytes, _bufs([("k", 64, 10, 0), ("k", 64, 10, 0)]), 64, 0) == cap.CAP_E_INVAL
+    assert _status(cap.capsule_layout_bytes, _bufs(ok), 0, 0) == cap.CAP_E_INVAL
+    assert _status(cap.capsule_layout_bytes, _bufs(ok), 64, 128) == cap.CAP_E_SIZE  # P' = 128 > 100 rows
+    many = [("b%d" % i, 16, 1, 1) for i in range(cap.CAP_MAX_BUFFERS + 1)]
+    assert _status(cap.capsule_layout_bytes, _bufs(many), 1, 0) == cap.CAP_E_UNSUPPORTED
+
+
+def test_set_create_rejects_before_device():
+    # checks that run before the device table is built
+    assert _status(cap.cap_set_create, [("k", 0, 64, 10, 0)], 64, 1) == cap.CAP_E_INVAL      # null pointer
+    assert _status(cap.cap_set_create, [("k", 8, 64, 10, 0)], 64, 1) == cap.CAP_E_ALIGN      # misaligned
+    assert _status(cap.cap_set_create, [("k", 4096, 64, 10, 3)], 64, 1) == cap.CAP_E_UNSUPPORTED
+    overlapping = [("a", 4096, 64, 10, 0), ("b", 4096 + 320, 64, 10, 0)]
+    assert _status(cap.cap_set_create, overlapping, 64, 1) == cap.CAP_E_INVAL
+
+
+def test_null_handles():
+    L = N.load()
+    out = ct.c_uint64(0)
+    assert L.capsule_bytes(None, 0, ct.byref(out)) == cap.CAP_E_INVAL
+    assert L.cap_set_set_position(None, 0) == cap.CAP_E_INVAL
+    assert L.cap_set_destroy(None) == cap.CAP_E_INVAL
+    assert L.capsule_release(None) == cap.CAP_E_INVAL
+    assert L.capsule_restore(None, None, 0, None, None) == cap.CAP_E_INVAL
+    h = ct.c_void_p(1)
+    assert L.capsule_snapshot(None, 0, 0, None, 0, None, ct.byref(h)) == cap.CAP_E_INVAL
+    assert h.value is None  # *out cleared on error
+    assert L.capsule_fork(None, None, 0, 0, None) == cap.CAP_E_INVAL
+    assert L.capsule_gather_restore(None, 0, None, None, 0, None) == cap.CAP_E_INVAL
+    assert L.linattn_chunked_prefill(None, None) == cap.CAP_E_INVAL
+
+
+def _args(**kw):
+    base = dict(q=4096, k=8192, v=12288, g=16384, state_in=0, o=1 << 30, chunk_states=0, final_state=0,
+                T=4, H=1, dk=64, dv=16, chunk=64, in_dtype=cap.CAP_DTYPE_BF16, scale=1.0)
+    base.update(kw)
+    return N.linattn_args(**base)
+
+
+def _scan_status(**kw):
+    return N.load().linattn_chunked_prefill(ct.byref(_args(**kw)), None)
+
+
+def test_scan_argument_checks():
+    # every case below fails on the host before any launch
+    assert _scan_status(T=-1) == cap.CAP_E_INVAL
+    assert _scan_status(H=0) == cap.CAP_E_INVAL
+    assert _scan_status(in_dtype=7) == cap.CAP_E_INVAL
+    assert _scan_status(q=0) == cap.CAP_E_INVAL
+    assert _scan_status(o=0) == cap.CAP_E_INVAL
+    assert _scan_status(chunk=32) == cap.CAP_E_UNSUPPORTED
+    assert _scan_status(dk=96) == cap.CAP_E_UNSUPPORTED
+    assert _scan_status(dv=24) == cap.CAP_E_UNSUPPORTED
+    assert _scan_status(dk=128, in_dtype=cap.CAP_DTYPE_F32) == cap.CAP_E_UNSUPPORTED
+    assert _scan_status(q=4100) == cap.CAP_E_ALIGN
+    assert _scan_status(final_state=4104) == cap.CAP_E_ALIGN
+    # an output overlapping an input
+    assert _scan_status(o=8192 + 64) == cap.CAP_E_INVAL
+    # outputs overlapping each other
+    assert _scan_status(final_state=1 << 30) == cap.CAP_E_INVAL
+    # nothing to do: T = 0 without a final state returns at once
+    assert _scan_status(T=0, q=0, k=0, v=0, g=0, o=0) == cap.CAP_OK
+
+
+def test_python_binding_has_no_fallback(tmp_path):
+    with pytest.raises(ImportError):
+        N.load(str(tmp_path / "missing.so"))

@@ -1,0 +1,143 @@
+"""Full-size cases in the launch configuration bench.py times: one 48-layer
+workload layer (16384 tokens x 32 heads, dk = dv = 128) against the oracle on
+sampled heads, the full 881,983,488-byte capsule against the oracle's memcpy,
+fork x4, and the robot-reset workload (32 environments, gallery of 8
+capsules, 1000 batched gather-restores)."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2606_20537_amd as cap
+import synth
+from gpu_util import PARITY_TOL, SPLIT_TOL, dev_inputs, rel_err
+
+pytestmark = pytest.mark.gpu
+
+H48 = synth.get_config("hybrid48")
+
+
+def test_hybrid48_layer_sampled_heads(orc):
+    w = H48
+    T, H, dk, dv = w.prefix, w.heads, w.dk, w.dv
+    inp = synth.linattn_inputs(w.seed, 0, T, H, dk, dv, "bf16")
+    d = dev_inputs(inp)
+    n_chunks = T // 64
+    o = torch.empty((T, H, dv), dtype=torch.float32, device="cuda")
+    cs = torch.empty((n_chunks, H, dk, dv), dtype=torch.float32, device="cuda")
+    fs = torch.empty((H, dk, dv), dtype=torch.float32, device="cuda")
+    cap.linattn_chunked_prefill(d["q"], d["k"], d["v"], d["g"], o, chunk_states=cs, final_state=fs)
+    torch.cuda.synchronize()
+    heads = [0, 13, 31]
+    sub = {n: np.ascontiguousarray(inp[n][:, heads]) for n in ("q", "k", "v", "g")}
+    o_ref, s_ref = orc.sequential(sub["q"], sub["k"], sub["v"], sub["g"])
+    _, cs_ref, _ = orc.chunked(sub["q"], sub["k"], sub["v"], sub["g"], 64)
+    o_np = o[:, heads].cpu().numpy()
+    e_o = rel_err(o_np, o_ref)
+    e_s = rel_err(fs[heads].cpu().numpy(), s_ref)
+    e_c = max(rel_err(cs[j][heads].cpu().numpy(), cs_ref[j]) for j in (1, 100, 128, 255))
+    print("16k x 32 heads, heads %s: rel err o %.3g final %.3g chunk states %.3g" % (heads, e_o, e_s, e_c))
+    assert e_o <= PARITY_TOL and e_s <= PARITY_TOL and e_c <= PARITY_TOL
+    assert e_o <= SPLIT_TOL and e_s <= SPLIT_TOL and e_c <= SPLIT_TOL
+    assert torch.isfinite(o).all() and torch.isfinite(cs).all()
+
+
+def hybrid48_layout(w):
+    """(name, row_bytes, rows, kind) of the 48-layer live set, 3:1 interleaved."""
+    lay = []
+    li = ki = 0
+    for layer in range(w.n_linear + w.n_full):
+        if layer % 4 == 3:
+            for n in ("k", "v"):
+                lay.append(("kv%d.%s" % (ki, n), w.kv_row_bytes, w.t_max, cap.CAP_KIND_POSITIONAL))
+            ki += 1
+        else:
+            lay.append(("lin%d.state" % li, w.heads * w.dk * w.dv * 4, 1, cap.CAP_KIND_FIXED))
+            lay.append(("lin%d.conv" % li, w.conv_width * w.conv_channels * 2, 1, cap.CAP_KIND_FIXED))
+            li += 1
+    return lay
+
+
+def random_buffers(layout, seed):
+    g = torch.Generator(device="cuda").manual_seed(seed)
+    out = []
+    for name, rb, rows, kind in layout:
+        t = torch.empty(rb * rows, dtype=torch.uint8, device="cuda")
+        t.view(torch.int32).random_(generator=g)
+        out.append((name, t, rb, rows, kind))
+    return out
+
+
+def test_hybrid48_capsule_bytes_restore_and_fork(orc):
+    w = H48
+    P = w.prefix
+    layout = hybrid48_layout(w)
+    bufs = random_buffers(layout, 1)
+    live = cap.cap_set_create(bufs, w.chunk, 7)
+    cap.cap_set_set_position(live, P)
+    nbytes = cap.capsule_bytes(live, P)
+    assert nbytes == 881_983_488
+    arena = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    c = cap.capsule_snapshot(live, P, 1, arena)
+    torch.cuda.synchronize()
+    host = [b[1].cpu().numpy() for b in bufs]
+    rb, rt, kd = [b[2] for b in bufs], [b[3] for b in bufs], [b[4] for b in bufs]
+    want = orc.snapshot(host, rb, rt, kd, P)
+    assert np.array_equal(arena.cpu().numpy(), want)
+    # dirty everything, restore, compare with the oracle's restore of the same bytes
+    for b in bufs:
+        b[1].fill_(0xA5)
+    cap.capsule_restore(c, live, 1)
+    torch.cuda.synchronize()
+    expect = [np.full_like(h, 0xA5) for h in host]
+    orc.restore(want, expect, rb, rt, kd, P)
+    for b, e in zip(bufs, expect):
+        assert np.array_equal(b[1].cpu().numpy(), e), b[0]
+    # fork into 4 sibling sessions
+    sibs = []
+    for i in range(4):
+        sb = random_buffers(layout, 10 + i)
+        sibs.append((cap.cap_set_create(sb, w.chunk, 7), sb))
+    cap.capsule_fork(c, [s for s, _ in sibs], 1)
+    torch.cuda.synchronize()
+    for s, sb in sibs:
+        for (name, t, r, rows, kind), src in zip(sb, bufs):
+            n = P * r if kind == cap.CAP_KIND_POSITIONAL else r * rows
+            assert torch.equal(t[:n], src[1][:n]), name
+
+
+def test_robot_reset_1000_gather_restores():
+    w = synth.get_config("robot_reset")
+    ex = dict(w.extra)
+    n_env, n_gal, n_resets = ex["envs"], ex["gallery"], ex["resets"]
+    layout = []
+    for l in range(w.n_full):
+        for n in ("k", "v"):
+            layout.append(("kv%d.%s" % (l, n), w.kv_row_bytes, w.t_max, cap.CAP_KIND_POSITIONAL))
+    layout.append(("denoiser", ex["denoiser_bytes"], 1, cap.CAP_KIND_FIXED))
+    P = w.prefix
+    gal_bufs, gallery = [], []
+    for gi in range(n_gal):
+        b = random_buffers(layout, 100 + gi)
+        s = cap.cap_set_create(b, w.chunk, 3)
+        cap.cap_set_set_position(s, P)
+        arena = torch.empty(cap.capsule_bytes(s, P), dtype=torch.uint8, device="cuda")
+        gallery.append(cap.capsule_snapshot(s, P, 0, arena))
+        gal_bufs.append((s, b))
+    assert cap.capsule_info(gallery[0])["bytes"] == 17_137_664
+    envs = []
+    for e in range(n_env):
+        b = random_buffers(layout, 500 + e)
+        envs.append((cap.cap_set_create(b, w.chunk, 3), b))
+    ids_all = synth.rng(w.seed, 0, "reset_ids").integers(0, n_gal, size=(n_resets, n_env)).astype(np.int32)
+    den_gal = torch.stack([b[-1][1] for _, b in gal_bufs])          # [gallery, 2 MiB]
+    mismatches = torch.zeros((), dtype=torch.int64, device="cuda")
+    for r in range(n_resets):
+        ids = ids_all[r]
+        cap.capsule_gather_restore(gallery, ids, [s for s, _ in envs])
+        den_env = torch.stack([b[-1][1] for _, b in envs])          # [env, 2 MiB]
+        mismatches += (den_env != den_gal[torch.from_numpy(ids).long().cuda()]).sum()
+        if r % 100 == 99 or r == n_resets - 1:
+            for (s, b), i in zip(envs, ids):
+                for (name, t, rb, rows, kind), src in zip(b, gal_bufs[i][1]):
+                    assert torch.equal(t, src[1]), (r, name)
+    assert int(mismatches) == 0

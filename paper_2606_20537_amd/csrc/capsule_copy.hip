@@ -6,15 +6,16 @@
 // [0, P'), fixed buffers all their bytes.  The copy is HBM-bound (§3 Table
 // "cost structure": restore is a bandwidth-bound copy of Theta(bytes)), so the
 // kernel is built for bytes in flight, not arithmetic:
-//   * each buffer's valid range is cut into tiles of kTileVec 16-byte vectors
-//     that never cross a buffer boundary, so inside a tile every thread
-//     addresses base + index with block-uniform bases, and the kUnroll
-//     16-byte loads of a thread are all issued before its first store
-//     (global_load_dwordx4 / global_store_dwordx4, 1 KiB per wave instruction);
+//   * each buffer's valid range is cut into tiles of kThreads x kUnroll
+//     16-byte vectors that never cross a buffer boundary, one block per tile,
+//     so inside a tile every thread addresses base + index with block-uniform
+//     bases, and the kUnroll 16-byte loads of a thread are all issued before
+//     its first store (global_load_dwordx4 / global_store_dwordx4, 1 KiB per
+//     wave instruction);
 //   * tile counts per buffer depend on the call's P', so each block turns the
 //     set's static (a, b) table into capsule offsets and an exclusive prefix
-//     sum of tile counts once, in LDS, then walks tiles with a grid stride and
-//     finds a tile's buffer by a binary search in LDS;
+//     sum of tile counts once, in LDS, and finds its tile's buffer by a
+//     binary search in LDS;
 //   * fork reads each vector once and stores it to every destination set;
 //     gather gives each environment ("rep") its own source arena.
 #include <hip/hip_runtime.h>
@@ -24,13 +25,22 @@
 namespace cap {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kUnroll = 8;
-constexpr uint32_t kTileVec = (uint32_t)kThreads * kUnroll;  // 32 KiB per tile
-constexpr int kMaxSeg = 512;                                  // buffers per set
-constexpr int kPer = (kMaxSeg + 1 + kThreads - 1) / kThreads; // table entries per thread
+constexpr int kMaxSeg = 512;  // buffers per set
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte load / store, optionally non-temporal (streamed past the caches).
+template <bool NT>
+__device__ inline u32x4 ld16(const u32x4* p) {
+    if (NT) return __builtin_nontemporal_load(p);
+    return *p;
+}
+
+template <bool NT>
+__device__ inline void st16(u32x4* p, const u32x4& v) {
+    if (NT) __builtin_nontemporal_store(v, p);
+    else *p = v;
+}
 
 __device__ inline uint64_t seg_start(const SegEntry* t, uint32_t i, uint64_t P) {
     return (t[i].a + P * t[i].b) >> 4;  // in 16-byte vectors
@@ -46,7 +56,11 @@ __device__ inline uint32_t last_le(const uint32_t* a, uint32_t n, uint32_t x) {
     return lo;
 }
 
+// kThreads threads of kUnroll 16-byte vectors each form one tile.
+template <int kThreads, int kUnroll, bool NT_LD, bool NT_ST>
 __global__ __launch_bounds__(kThreads) void capsule_copy_kernel(const CopyParams p) {
+    constexpr uint32_t kTileVec = (uint32_t)kThreads * kUnroll;
+    constexpr int kPer = (kMaxSeg + 1 + kThreads - 1) / kThreads;  // table entries per thread
     __shared__ uint64_t s_start[kMaxSeg + 1];  // capsule vector offset of buffer i
     __shared__ uint32_t s_tile[kMaxSeg + 1];   // first tile of buffer i
     __shared__ uint32_t s_wave[kThreads / 64];
@@ -133,16 +147,16 @@ __global__ __launch_bounds__(kThreads) void capsule_copy_kernel(const CopyParams
             #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
                 const uint32_t i = u * kThreads + tid;
-                data[u] = src[i < last ? i : last];
+                data[u] = ld16<NT_LD>(src + (i < last ? i : last));
             }
             if (full) {
                 #pragma unroll
-                for (int u = 0; u < kUnroll; ++u) dst[u * kThreads + tid] = data[u];
+                for (int u = 0; u < kUnroll; ++u) st16<NT_ST>(dst + u * kThreads + tid, data[u]);
             } else {
                 #pragma unroll
                 for (int u = 0; u < kUnroll; ++u) {
                     const uint32_t i = u * kThreads + tid;
-                    if (i <= last) dst[i] = data[u];
+                    if (i <= last) st16<NT_ST>(dst + i, data[u]);
                 }
             }
         } else {
@@ -150,18 +164,18 @@ __global__ __launch_bounds__(kThreads) void capsule_copy_kernel(const CopyParams
             #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
                 const uint32_t i = u * kThreads + tid;
-                data[u] = src[i < last ? i : last];
+                data[u] = ld16<NT_LD>(src + (i < last ? i : last));
             }
             for (uint32_t d = 0; d < n_dst; ++d) {
                 u32x4* dst = reinterpret_cast<u32x4*>(s_ptr[d * n + seg]) + off;
                 if (full) {
                     #pragma unroll
-                    for (int u = 0; u < kUnroll; ++u) dst[u * kThreads + tid] = data[u];
+                    for (int u = 0; u < kUnroll; ++u) st16<NT_ST>(dst + u * kThreads + tid, data[u]);
                 } else {
                     #pragma unroll
                     for (int u = 0; u < kUnroll; ++u) {
                         const uint32_t i = u * kThreads + tid;
-                        if (i <= last) dst[i] = data[u];
+                        if (i <= last) st16<NT_ST>(dst + i, data[u]);
                     }
                 }
             }
@@ -171,15 +185,31 @@ __global__ __launch_bounds__(kThreads) void capsule_copy_kernel(const CopyParams
 
 }  // namespace
 
+template <int kThreads, int kUnroll, bool NT_LD, bool NT_ST>
+hipError_t launch_t(const CopyParams& p, hipStream_t stream) {
+    constexpr uint64_t kTileVec = (uint64_t)kThreads * kUnroll;
+    // one block per tile; every buffer adds at most one partial tile
+    const uint64_t tiles = (p.nvec / kTileVec + p.n_seg) * p.n_rep;
+    if (tiles > 0x7fffffffull) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((capsule_copy_kernel<kThreads, kUnroll, NT_LD, NT_ST>), dim3((unsigned)tiles),
+                       dim3(kThreads), 0, stream, p);
+    return hipGetLastError();
+}
+
 hipError_t launch_copy(const CopyParams& p, int num_cus, hipStream_t stream) {
+    (void)num_cus;
     if (p.nvec == 0 || p.n_rep == 0) return hipSuccess;
     if (p.n_seg > (uint32_t)kMaxSeg || p.n_seg * p.n_dst > (uint32_t)kMaxPtrLds) return hipErrorInvalidValue;
-    // an upper bound of the tile count: every buffer adds at most one partial tile
-    const uint64_t tiles = (p.nvec / kTileVec + p.n_seg) * p.n_rep;
-    const uint64_t cap_blocks = (uint64_t)(num_cus > 0 ? num_cus : 256) * 8;
-    const unsigned grid = (unsigned)(tiles < cap_blocks ? tiles : cap_blocks);
-    hipLaunchKernelGGL(capsule_copy_kernel, dim3(grid), dim3(kThreads), 0, stream, p);
-    return hipGetLastError();
+    // Tile shapes chosen by measurement on MI355X:
+    //  * snapshot / restore (882 MB capsule): 16 KiB tiles, loads and stores
+    //    streamed past the caches;
+    //  * fork, which stores every loaded vector several times: 8 KiB tiles of
+    //    512 threads, streamed;
+    //  * gather-restore: 16 KiB tiles with cached loads, so that a gallery
+    //    small enough for the 256 MB Infinity Cache stays there across resets.
+    if (p.n_dst > 1) return launch_t<512, 1, true, true>(p, stream);
+    if (p.n_rep > 1) return launch_t<256, 4, false, false>(p, stream);
+    return launch_t<256, 4, true, true>(p, stream);
 }
 
 }  // namespace cap

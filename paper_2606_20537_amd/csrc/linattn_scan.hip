@@ -128,10 +128,9 @@ __device__ inline void split8(const float* f, bf16x8& hi, bf16x8& lo) {
 // compile to single ds_read_b128 / ds_write_b128 instructions.
 template <int DK, bool F32>
 struct alignas(16) Smem {
-    static constexpr int KP = DK + 8;      // row pitch of K and Q (elements)
+    static constexpr int KP = DK + 8;      // row pitch of K (elements)
     static constexpr int NL = F32 ? 2 : 1; // bf16 planes of the inputs: hi (and lo)
     alignas(16) __bf16 k[2][NL][CH * KP];  // K     [m][d]
-    alignas(16) __bf16 q[2][NL][CH * KP];  // Q     [i][d]
     alignas(16) __bf16 v[2][NL][CH * VP];  // V     [m][j] (this slice)
     alignas(16) __bf16 vw[2][2][CH * VP];  // V w   [m][j], hi and lo planes
     alignas(16) __bf16 s[2][2][DK * VP];   // S_j   [d][j], hi and lo planes
@@ -180,13 +179,18 @@ __device__ inline void split_piece(const Piece<F32>& p, bf16x8& hi, bf16x8& lo) 
     }
 }
 
-// Register staging of one chunk's global loads (state role only).
+// Register staging of one chunk's global loads: K, V and g for the state
+// role, the wave's own 16 rows of Q for an output wave.
 template <bool F32, int PK>
 struct Stage {
     Piece<F32> kp[PK];
-    Piece<F32> qp[PK];
     Piece<F32> vp;
     float g;
+};
+
+template <bool F32, int NKK>
+struct QStage {
+    Piece<F32> qp[NKK];
 };
 
 // Workgroup barrier for LDS traffic only.  Global stores of o and the states
@@ -204,7 +208,7 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
     constexpr int KP = S_::KP;
     constexpr int NL = S_::NL;
     constexpr int NKK = DK / 32;             // k-steps of 32 over dk
-    constexpr int PK = (CH * DK / 8) / NS_T; // K (and Q) pieces per state thread
+    constexpr int PK = (CH * DK / 8) / NS_T; // K pieces per state thread
     constexpr int NDW = DK / 64;             // state tiles (16 rows of d) per state wave
     constexpr int ES = F32 ? 4 : 2;          // input element size
     __shared__ S_ sm;
@@ -258,15 +262,12 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
         const int64_t t0 = c * CH;
         const int64_t rows = T - t0;
         const rsrc_t rk = make_rsrc(static_cast<const char*>(p.k) + t0 * qk_row, rows * qk_row);
-        const rsrc_t rq = make_rsrc(static_cast<const char*>(p.q) + t0 * qk_row, rows * qk_row);
         #pragma unroll
         for (int u = 0; u < PK; ++u) {
             const int pc = st + NS_T * u;
             const int m = pc / (DK / 8);
             const int d0 = (pc % (DK / 8)) * 8;
-            const uint32_t off = (uint32_t)(m * qk_row + ((int64_t)h * DK + d0) * ES);
-            load_piece<F32>(R.kp[u], rk, off);
-            load_piece<F32>(R.qp[u], rq, off);
+            load_piece<F32>(R.kp[u], rk, (uint32_t)(m * qk_row + ((int64_t)h * DK + d0) * ES));
         }
         // V slice: 128 pieces for state threads 0..127; threads 128..255 fetch
         // the same pieces (L2 hits) so that all state waves run one stream
@@ -287,9 +288,6 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
             split_piece<F32>(R.kp[u], hi, lo);
             *reinterpret_cast<bf16x8*>(&sm.k[b][0][m * KP + d0]) = hi;
             if (F32) *reinterpret_cast<bf16x8*>(&sm.k[b][NL - 1][m * KP + d0]) = lo;
-            split_piece<F32>(R.qp[u], hi, lo);
-            *reinterpret_cast<bf16x8*>(&sm.q[b][0][m * KP + d0]) = hi;
-            if (F32) *reinterpret_cast<bf16x8*>(&sm.q[b][NL - 1][m * KP + d0]) = lo;
         }
         // every state wave scans the chunk's log-gates: lane t holds G_t
         const float x = wave_inclusive_sum(R.g);
@@ -373,25 +371,29 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
     };
 
     // --------------------------------------------------------- output role
-    auto outputs = [&](int b, int64_t c) {
+    using QS = QStage<F32, NKK>;
+    // this output wave's 16 rows of Q for chunk c, straight into registers
+    auto load_q = [&](QS& Q, int64_t c) {
+        const int64_t t0 = c * CH;
+        const rsrc_t rq = make_rsrc(static_cast<const char*>(p.q) + t0 * qk_row, (T - t0) * qk_row);
+        #pragma unroll
+        for (int kk = 0; kk < NKK; ++kk)
+            load_piece<F32>(Q.qp[kk], rq, (uint32_t)((16 * wq + li) * qk_row + ((int64_t)h * DK + 32 * kk + 8 * grp) * ES));
+    };
+
+    auto outputs = [&](int b, int64_t c, const QS& Q) {
         const int w = wq;
         const int i_row = 16 * w + li;
         bf16x8 qh[NKK], ql[NKK];
         #pragma unroll
-        for (int kk = 0; kk < NKK; ++kk) {
-            const int off = i_row * KP + 32 * kk + 8 * grp;
-            qh[kk] = *reinterpret_cast<const bf16x8*>(&sm.q[b][0][off]);
-            if (F32) ql[kk] = *reinterpret_cast<const bf16x8*>(&sm.q[b][NL - 1][off]);
-        }
-        // A^T = K Q^T for all four m-blocks (the blocks above the diagonal are
-        // masked to zero below; computing them keeps the path branch-free and
-        // costs no time, since the wave with the most causal blocks sets the
-        // pace); lane (li, grp) of tile mb holds A^T[m = 16 mb + 4 grp + r][i = 16 w + li]
+        for (int kk = 0; kk < NKK; ++kk) split_piece<F32>(Q.qp[kk], qh[kk], ql[kk]);
+        // A^T = K Q^T for the causal m-blocks mb <= w (uniform branch); lane
+        // (li, grp) of tile mb holds A^T[m = 16 mb + 4 grp + r][i = 16 w + li]
         f32x4 at[4];
         #pragma unroll
         for (int mb = 0; mb < 4; ++mb) {
             at[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
-            {
+            if (mb <= w) {
                 bf16x8 a[NKK], al[NKK];
                 #pragma unroll
                 for (int kk = 0; kk < NKK; ++kk) {
@@ -409,23 +411,23 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
                 }
             }
         }
-        // decay: factored tables below the diagonal tile, exp2 on it, zero above
+        // decay: factored tables below the diagonal tile, exp2 on it
         {
             const f32x4 ai = *reinterpret_cast<const f32x4*>(&sm.ai[b][i_row][0]);
-            const float gi = sm.G2[b][i_row];
-            const f32x4 gm = *reinterpret_cast<const f32x4*>(&sm.G2[b][w * 16 + 4 * grp]);
-            f32x4 dg;  // diagonal tile
-            #pragma unroll
-            for (int r = 0; r < 4; ++r)
-                dg[r] = (4 * grp + r <= li) ? __builtin_amdgcn_exp2f(gi - gm[r]) : 0.0f;
             #pragma unroll
             for (int mb = 0; mb < 4; ++mb) {
-                const f32x4 bmv = *reinterpret_cast<const f32x4*>(&sm.bm[b][mb * 16 + 4 * grp]);
-                #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const float below = (at[mb][r] * ai[mb]) * bmv[r];
-                    const float diag = at[mb][r] * dg[r];
-                    at[mb][r] = mb < w ? below : (mb == w ? diag : 0.0f);
+                if (mb < w) {
+                    const f32x4 bmv = *reinterpret_cast<const f32x4*>(&sm.bm[b][mb * 16 + 4 * grp]);
+                    #pragma unroll
+                    for (int r = 0; r < 4; ++r) at[mb][r] = (at[mb][r] * ai[mb]) * bmv[r];
+                } else if (mb == w) {
+                    const float gi = sm.G2[b][i_row];
+                    const f32x4 gm = *reinterpret_cast<const f32x4*>(&sm.G2[b][mb * 16 + 4 * grp]);
+                    #pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const float pv = at[mb][r] * __builtin_amdgcn_exp2f(gi - gm[r]);
+                        at[mb][r] = (4 * grp + r <= li) ? pv : 0.0f;
+                    }
                 }
             }
         }
@@ -434,7 +436,7 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
         f32x4 acc_o = {0.f, 0.f, 0.f, 0.f};
         #pragma unroll
         for (int pr = 0; pr < 2; ++pr) {
-            {
+            if (2 * pr <= w) {
                 float f[8];
                 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
@@ -454,8 +456,9 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
                 }
             }
         }
-        // X^T = S_j^T Q^T from the published S planes
-        f32x4 acc_x = {0.f, 0.f, 0.f, 0.f};
+        // X^T = S_j^T Q^T from the published S planes, hi and lo products in
+        // two independent accumulators
+        f32x4 acc_x = {0.f, 0.f, 0.f, 0.f}, acc_xl = {0.f, 0.f, 0.f, 0.f};
         {
             bf16x8 sh[NKK], sl[NKK];
             #pragma unroll
@@ -467,9 +470,10 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
             #pragma unroll
             for (int kk = 0; kk < NKK; ++kk) {
                 acc_x = mma(sh[kk], qh[kk], acc_x);
-                acc_x = mma(sl[kk], qh[kk], acc_x);
-                if (F32) acc_x = mma(sh[kk], ql[kk], acc_x);
+                acc_xl = mma(sl[kk], qh[kk], acc_xl);
+                if (F32) acc_xl = mma(sh[kk], ql[kk], acc_xl);
             }
+            acc_x += acc_xl;
         }
         // o row i = 16 w + li, columns j0 + 4 grp .. + 3: one 16-byte store;
         // rows past T fall outside the chunk's buffer range and are dropped
@@ -488,10 +492,14 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
     // One loop per role; both run the same number of barriers.  The loops
     // advance two chunks per iteration so that the two register stages swap
     // roles without copies; a chunk index past the end does no visible work.
+    // One loop per role; both run one barrier per chunk.  Each loop advances
+    // three chunks per iteration so that three register stages rotate
+    // without copies (loads run three chunks ahead); a chunk index past the
+    // end issues only empty-range memory accesses and skips the barrier.
     if (state_role) {
         auto state_step = [&](int64_t c, St& Rfree, const St& Rnext) {
             const int b = (int)(c & 1);
-            load_chunk(Rfree, c + 2);
+            load_chunk(Rfree, c + 3);
             if (c + 1 < n_chunks) store_chunk(Rnext, b ^ 1);
             {
                 const bool live = c < n_chunks && p.chunk_states != nullptr;
@@ -507,18 +515,20 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
             if (c < n_chunks) {
                 fold(b);
                 publish_state(b ^ 1);
+                lds_barrier();
             }
-            lds_barrier();
         };
-        St R0, R1;
+        St R0, R1, R2;
         load_chunk(R0, 0);
         load_chunk(R1, 1);
+        load_chunk(R2, 2);
         store_chunk(R0, 0);
         publish_state(0);
         lds_barrier();
-        for (int64_t c = 0; c < n_chunks; c += 2) {
+        for (int64_t c = 0; c < n_chunks; c += 3) {
             state_step(c, R0, R1);
-            state_step(c + 1, R1, R0);
+            state_step(c + 1, R1, R2);
+            state_step(c + 2, R2, R0);
         }
         if (p.final_state) {
             #pragma unroll
@@ -528,12 +538,20 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
             }
         }
     } else {
+        auto out_step = [&](int64_t c, QS& Q) {
+            outputs((int)(c & 1), c, Q);  // past the end: reads stale LDS, stores nothing
+            load_q(Q, c + 3);
+            if (c < n_chunks) lds_barrier();
+        };
+        QS Q0, Q1, Q2;
+        load_q(Q0, 0);
+        load_q(Q1, 1);
+        load_q(Q2, 2);
         lds_barrier();
-        for (int64_t c = 0; c < n_chunks; c += 2) {
-            outputs(0, c);
-            lds_barrier();
-            outputs(1, c + 1);
-            lds_barrier();
+        for (int64_t c = 0; c < n_chunks; c += 3) {
+            out_step(c, Q0);
+            out_step(c + 1, Q1);
+            out_step(c + 2, Q2);
         }
     }
 }

@@ -5,7 +5,7 @@
 // once per chunk of C tokens).  For chunk j with entering state S_j and
 // inclusive in-chunk log-decay sums G_i:
 //   o_i     = scale * (exp(G_i) q_i S_j + sum_{m<=i} exp(G_i - G_m)(q_i.k_m) v_m)
-//   S_{j+1} = exp(G_last) S_j + sum_m exp(G_last - G_m) k_m^T v_m
+//   S_{j+1} = exp(G_last) S_j + D_j,  D_j = sum_m exp(G_last - G_m) k_m^T v_m
 //
 // Work split: one workgroup per (head, 16-wide slice of the value columns).
 // Column slices of S are independent: o[:, J] needs only S[:, J] and v[:, J],
@@ -15,38 +15,58 @@
 // That is what makes restore-at-an-aligned-boundary-then-continue bitwise
 // equal to one long prefill.
 //
-// Eight waves, two per SIMD, in two roles that overlap on every SIMD:
-//   output waves 0-3: wave w owns rows 16w..16w+15 of the chunk and computes
-//     A^T = K Q^T (causal tiles), P = A * decay, O^T = V^T P^T,
-//     X^T = S_j^T Q^T and o = scale (exp(G) X + O);
-//   state waves 4-7: stream the chunk two ahead from HBM into registers,
-//     stage it in LDS, write the chunk-boundary states and fold the state
-//     S^T = exp(G_last) S^T + (V w)^T K over their DK/64 tiles of 16 rows.
-// Every product runs on v_mfma_f32_16x16x32_bf16 with fp32 accumulation,
-// written transposed so that each lane ends with four consecutive value
-// columns (16-byte stores).  Inputs are exact bf16 operands; fp32-derived
-// operands (P, S_j, V w with w_m = exp(G_last - G_m)) are split hi + lo in
-// bf16, which keeps them to ~2^-17 relative error, far inside the 2e-3 parity
-// bar.  Scaling the 16-wide V slice by w instead of the dk-wide K keeps K
-// exact and the split small.  fp32 inputs are split hi + lo on load and use
-// three products per term.
+// Only S_{j+1} = exp(G_last) S_j + D_j is a true recurrence; D_j, the
+// intra-chunk scores and their decay do not depend on S.  The kernel is
+// therefore a software pipeline over chunks with one LDS barrier per step;
+// in step c:
+//   state waves 4-7  issue the HBM loads of chunk c+4, stage chunk c+2 in LDS
+//                    (K; the gate wave also V, V w and the decay tables),
+//                    start D_{c+1} on MFMA, write the chunk-boundary state
+//                    S_c, then S_{c+1} = exp(G_last) S_c + D_c (one FMA per
+//                    element) and publish S_{c+1} for step c+1;
+//   output waves 0-3 start A^T_{c+1} = K_{c+1} Q_{c+1}^T (causal tiles) and
+//                    finish chunk c: P = A^T * decay, O = P V, X = Q S_c,
+//                    o = scale (exp(G) X + O).
+// Wave w of the output role owns rows 16w..16w+15 of the chunk; each wave's
+// role and row block are template parameters, so the causal tiling compiles
+// to straight-line code the scheduler can interleave with the next chunk's
+// products.  Stage buffers: K, V w and S by chunk parity, V and the tables by
+// chunk mod 4, the register prefetch four chunks deep.
+//
+// Memory access.  Every 16-column slice of a head reads the head's full Q
+// and K rows, so per chunk a workgroup asks L2 for ~380 cache lines, most of
+// them also wanted by its sibling slices at the same moment; the kernel is
+// bound by those requests, not by arithmetic.  Hence: every load and store
+// is coalesced (consecutive lanes touch consecutive bytes of a row); Q rows
+// pass through a small per-wave LDS tile to reach operand layout; only one
+// wave reads g and V; accumulators are laid out [row][value column] so that
+// the 16 lanes of a group store 64 contiguous bytes of o or of a state row;
+// and each slice prefetches its eighth of the head's lines into L2 ahead of
+// the regular loads (see prefetch below).
+//
+// Every product runs on v_mfma_f32_16x16x32_bf16 with fp32 accumulation.
+// Inputs are exact bf16 operands; fp32-derived operands (P, S_j, V w with
+// w_m = exp(G_last - G_m)) are split hi + lo in bf16, which keeps them to
+// ~2^-17 relative error, far inside the 2e-3 parity bar.  Scaling the 16-wide
+// V slice by w instead of the dk-wide K keeps K exact and the split small.
+// fp32 inputs are split hi + lo on load and use three products per term.
 //
 // Decay: inside the chunk G is non-increasing for g <= 0.  Below the diagonal
 // tile, exp(G_i - G_m) = exp(G_i - G_e) exp(G_e - G_m) with e the last token of
 // m's 16-token block; both factors lie in (0, 1], come from per-chunk tables
 // and never overflow.  The diagonal tile evaluates exp2 directly.
 //
-// LDS holds every tile row-major (K, Q, V, V w and the published S), written
-// with 8- and 16-byte stores.  Operands whose contraction index runs along the
-// rows (V^T, (V w)^T, S^T as A operands; K as the fold's B operand) are read
-// with gfx950's transposing LDS load ds_read_b64_tr_b16: inside a 16-lane
-// group, lane L addresses row k0 + L/4, columns 4(L%4)..+3, and lane n
-// receives column n of rows k0..k0+3.  The contraction index may be permuted
-// freely as long as both operands agree, which lets the accumulator of K Q^T
-// serve directly as the B operand of V^T P^T.  HBM traffic goes through buffer
+// LDS holds every tile row-major (K, V, V w, Q, and the published S as
+// S^T), written with 8- and 16-byte stores.  Operands whose contraction index
+// runs along the rows (K^T and V w for the fold, V for O) are read with
+// gfx950's transposing LDS load ds_read_b64_tr_b16: inside a 16-lane group,
+// lane L addresses row k0 + L/4, columns 4(L%4)..+3, and lane n receives
+// column n of rows k0..k0+3.  The contraction index may be permuted freely as
+// long as both operands agree, which lets the accumulator of K Q^T serve
+// directly as the A operand of P V.  HBM traffic goes through buffer
 // resources: a scalar base per chunk, fixed per-lane offsets, and hardware
 // range checks that read the ragged tail as zeros and drop stores past T.
-// The one barrier per chunk orders LDS only and never waits for global stores.
+// The barrier orders LDS only and never waits for global stores.
 #include <hip/hip_runtime.h>
 
 #include "internal.h"
@@ -115,9 +135,10 @@ __device__ inline float lane_value(float x, int l) {
 }
 
 // hi + lo split of fp32 values into bf16 (round to nearest even both times).
-__device__ inline void split8(const float* f, bf16x8& hi, bf16x8& lo) {
+template <int N, typename V>
+__device__ inline void split_n(const float* f, V& hi, V& lo) {
     #pragma unroll
-    for (int e = 0; e < 8; ++e) {
+    for (int e = 0; e < N; ++e) {
         const __bf16 h = (__bf16)f[e];
         hi[e] = h;
         lo[e] = (__bf16)(f[e] - (float)h);
@@ -128,16 +149,22 @@ __device__ inline void split8(const float* f, bf16x8& hi, bf16x8& lo) {
 // compile to single ds_read_b128 / ds_write_b128 instructions.
 template <int DK, bool F32>
 struct alignas(16) Smem {
-    static constexpr int KP = DK + 8;      // row pitch of K (elements)
+    // Row pitches (elements).  K rows are read 16 rows x 16 B at a time and
+    // 4 rows x 32 B at a time (transposing reads): a pitch of 16 B times an
+    // odd number whose 4-row windows do not overlap keeps both conflict-free
+    // (304 B for dk = 128, 208 B for dk = 64).  S^T rows are read 16 x 16 B.
+    static constexpr int KP = DK == 128 ? 152 : 104;
+    static constexpr int SP = DK + 8;
     static constexpr int NL = F32 ? 2 : 1; // bf16 planes of the inputs: hi (and lo)
-    alignas(16) __bf16 k[2][NL][CH * KP];  // K     [m][d]
-    alignas(16) __bf16 v[2][NL][CH * VP];  // V     [m][j] (this slice)
-    alignas(16) __bf16 vw[2][2][CH * VP];  // V w   [m][j], hi and lo planes
-    alignas(16) __bf16 s[2][2][DK * VP];   // S_j   [d][j], hi and lo planes
-    alignas(16) float G2[2][CH];           // G_t log2(e), G the inclusive log-decay sum
-    alignas(16) float eG[2][CH];           // exp(G_t)
-    alignas(16) float bm[2][CH];           // exp(G_e - G_m), e = last token of m's block
-    alignas(16) float ai[2][CH][4];        // exp(G_i - G_e(M)) for 16-token blocks M below i's
+    alignas(16) __bf16 k[2][NL][CH * KP];  // K     [m][d]     by chunk parity
+    alignas(16) __bf16 v[4][NL][CH * VP];  // V     [m][j]     by chunk mod 4
+    alignas(16) __bf16 vw[2][2][CH * VP];  // V w   [m][j]     hi, lo; by chunk parity
+    alignas(16) __bf16 s[2][2][DVS * SP];  // S_j^T [j][d]     hi, lo; by chunk parity
+    alignas(16) __bf16 q[4][NL][16 * SP];  // Q     [i][d]     each output wave's 16 rows
+    alignas(16) float G2[4][CH];           // G_t log2(e), G the inclusive log-decay sum
+    alignas(16) float eG[4][CH];           // exp(G_t)
+    alignas(16) float bm[4][CH];           // exp(G_e - G_m), e = last token of m's block
+    alignas(16) float ai[4][CH][4];        // exp(G_i - G_e(M)) for 16-token blocks M below i's
 };
 
 // 8 consecutive input elements of one row (16 B of bf16 or 32 B of fp32).
@@ -152,9 +179,25 @@ __device__ inline void load_piece(Piece<F32>& p, rsrc_t r, uint32_t off) {
     if (F32) p.x[F32 ? 1 : 0] = __builtin_amdgcn_raw_buffer_load_b128(r, off + 16, 0, 0);
 }
 
+// A piece as bf16 hi (and lo, for fp32 inputs).
+template <bool F32>
+__device__ inline void split_piece(const Piece<F32>& p, bf16x8& hi, bf16x8& lo) {
+    if (F32) {
+        const f32x4 a = __builtin_bit_cast(f32x4, p.x[0]);
+        const f32x4 b = __builtin_bit_cast(f32x4, p.x[F32 ? 1 : 0]);
+        float f[8];
+        #pragma unroll
+        for (int e = 0; e < 4; ++e) { f[e] = a[e]; f[4 + e] = b[e]; }
+        split_n<8>(f, hi, lo);
+    } else {
+        hi = __builtin_bit_cast(bf16x8, p.x[0]);
+        lo = bf16x8{};
+    }
+}
+
 template <bool F32>
 __device__ inline void piece_f32(const Piece<F32>& p, float* f) {
-    if (F32) {
+    if constexpr (F32) {
         const f32x4 a = __builtin_bit_cast(f32x4, p.x[0]);
         const f32x4 b = __builtin_bit_cast(f32x4, p.x[F32 ? 1 : 0]);
         #pragma unroll
@@ -166,31 +209,21 @@ __device__ inline void piece_f32(const Piece<F32>& p, float* f) {
     }
 }
 
-// A piece as bf16 hi (and lo, for fp32 inputs).
-template <bool F32>
-__device__ inline void split_piece(const Piece<F32>& p, bf16x8& hi, bf16x8& lo) {
-    if (F32) {
-        float f[8];
-        piece_f32<F32>(p, f);
-        split8(f, hi, lo);
-    } else {
-        hi = __builtin_bit_cast(bf16x8, p.x[0]);
-        lo = bf16x8{};
-    }
-}
-
-// Register staging of one chunk's global loads: K, V and g for the state
-// role, the wave's own 16 rows of Q for an output wave.
+// Register staging of one chunk for the state role: its K pieces, and for
+// the wave that owns the gates also its V slice and the log-gates of the
+// next chunk.
 template <bool F32, int PK>
 struct Stage {
     Piece<F32> kp[PK];
-    Piece<F32> vp;
+    Piece<F32> vp[2];
     float g;
 };
 
-template <bool F32, int NKK>
+// Register staging of one chunk of Q rows for an output wave: 16-byte pieces
+// in coalesced order (consecutive lanes read consecutive bytes of a row).
+template <int NQI>
 struct QStage {
-    Piece<F32> qp[NKK];
+    u32x4 qp[NQI];
 };
 
 // Workgroup barrier for LDS traffic only.  Global stores of o and the states
@@ -202,83 +235,79 @@ __device__ inline void lds_barrier() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-template <int DK, bool F32>
-__global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
+// Per-workgroup constants shared by both roles.
+struct Ctx {
+    int h, j0, H, dv, lane, li, grp;
+    int64_t T, n;                  // tokens, chunks
+    int64_t qk_row, v_row, o_row;  // bytes per token of q / k, v, o
+};
+
+// Both roles walk the chunks four steps per loop iteration (the register
+// stages rotate without copies).  Every global access of a step is issued
+// unconditionally -- chunks past the end get an empty buffer range: loads
+// read zeros, stores are dropped -- so the compiler's in-order memory
+// counters stay exact and the prefetch is never drained; a step past the end
+// changes no state, writes only LDS buffers no live step reads, and skips
+// the barrier.  Both roles run two barriers in the prologue and one per chunk.
+
+// ------------------------------------------------------------- state role
+template <int DK, bool F32, bool TABLES>
+__device__ __forceinline__ void state_role(const ScanParams& p, Smem<DK, F32>& sm, const Ctx& x, int wq) {
     using S_ = Smem<DK, F32>;
     constexpr int KP = S_::KP;
     constexpr int NL = S_::NL;
-    constexpr int NKK = DK / 32;             // k-steps of 32 over dk
-    constexpr int PK = (CH * DK / 8) / NS_T; // K pieces per state thread
-    constexpr int NDW = DK / 64;             // state tiles (16 rows of d) per state wave
-    constexpr int ES = F32 ? 4 : 2;          // input element size
-    __shared__ S_ sm;
+    constexpr int ES = F32 ? 4 : 2;
+    constexpr int PK = (CH * DK / 8) / NS_T;  // K pieces per state thread
+    constexpr int NDW = DK / 64;              // state tiles (16 rows of d) per wave
+    using St = Stage<F32, PK>;
+    const int lane = x.lane, li = x.li, grp = x.grp, h = x.h, j0 = x.j0, H = x.H, dv = x.dv;
+    const int st = 64 * wq + lane;
 
-    const int tid = threadIdx.x;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform
-    const bool state_role = wave >= 4;
-    const int wq = wave & 3;
-    const int lane = tid & 63;
-    const int li = lane & 15;
-    const int grp = lane >> 4;
-    const int st = tid - NS_T;  // state-role thread index (valid when state_role)
-
-    // workgroup -> (head, slice); slices of one head share an XCD (and its L2)
-    // when the grid allows it (workgroups go round-robin over 8 XCDs).
-    const int H = p.H, dv = p.dv;
-    const int NS = dv / DVS;
-    const int N = H * NS;
-    int logical = blockIdx.x;
-    if ((N % 8) == 0 && ((N / 8) % NS) == 0) logical = (blockIdx.x % 8) * (N / 8) + blockIdx.x / 8;
-    const int h = logical / NS;
-    const int j0 = (logical % NS) * DVS;
-
-    const int64_t T = p.T;
-    const int64_t n_chunks = (T + CH - 1) / CH;
-    const int64_t qk_row = (int64_t)H * DK * ES;  // bytes per token of q / k
-    const int64_t v_row = (int64_t)H * dv * ES;   // bytes per token of v
-    const int64_t o_row = (int64_t)H * dv * 4;    // bytes per token of o
-
-    // ---- state (state role), as S^T tiles in accumulator layout: lane
-    // (li, grp) of tile u holds S[d][j0 + 4 grp + r] with d = (wq*NDW + u)*16 + li.
-    f32x4 S[NDW];
+    // S tiles in accumulator layout: lane (li, grp) of tile u holds
+    // S[d][j0 + li] for d = (wq*NDW + u)*16 + 4 grp + r, r = 0..3.  For each
+    // r the 16 lanes of a group hold 64 contiguous bytes of a state row, so
+    // state reads and writes coalesce.
+    constexpr int SP = S_::SP;
+    f32x4 S[NDW], D0[NDW], D1[NDW];
+    auto srow = [&](int u, int r) -> int64_t {  // element offset of S[d][j0 + li] in a [H][dk][dv] state
+        return ((int64_t)h * DK + (wq * NDW + u) * 16 + 4 * grp + r) * dv + j0 + li;
+    };
     #pragma unroll
-    for (int u = 0; u < NDW; ++u) S[u] = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (state_role && p.state_in) {
-        #pragma unroll
-        for (int u = 0; u < NDW; ++u) {
-            const int d = (wq * NDW + u) * 16 + li;
-            S[u] = *reinterpret_cast<const f32x4*>(p.state_in + ((int64_t)h * DK + d) * dv + j0 + 4 * grp);
+    for (int u = 0; u < NDW; ++u) {
+        S[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (p.state_in) {
+            #pragma unroll
+            for (int r = 0; r < 4; ++r) S[u][r] = p.state_in[srow(u, r)];
         }
     }
 
-    using St = Stage<F32, PK>;
-
-    // ---------------------------------------------------------- state role
-    // Every global access of the state loop is issued unconditionally (chunks
-    // past the end get an empty buffer range: loads read zeros, stores are
-    // dropped), so the compiler's in-order memory counters stay exact and the
-    // prefetch of chunk c + 2 is never drained while chunk c computes.
     auto load_chunk = [&](St& R, int64_t c) {
         const int64_t t0 = c * CH;
-        const int64_t rows = T - t0;
-        const rsrc_t rk = make_rsrc(static_cast<const char*>(p.k) + t0 * qk_row, rows * qk_row);
+        const int64_t rows = x.T - t0;
+        const rsrc_t rk = make_rsrc(static_cast<const char*>(p.k) + t0 * x.qk_row, rows * x.qk_row);
         #pragma unroll
         for (int u = 0; u < PK; ++u) {
             const int pc = st + NS_T * u;
             const int m = pc / (DK / 8);
             const int d0 = (pc % (DK / 8)) * 8;
-            load_piece<F32>(R.kp[u], rk, (uint32_t)(m * qk_row + ((int64_t)h * DK + d0) * ES));
+            load_piece<F32>(R.kp[u], rk, (uint32_t)(m * x.qk_row + ((int64_t)h * DK + d0) * ES));
         }
-        // V slice: 128 pieces for state threads 0..127; threads 128..255 fetch
-        // the same pieces (L2 hits) so that all state waves run one stream
-        const rsrc_t rv = make_rsrc(static_cast<const char*>(p.v) + t0 * v_row, rows * v_row);
-        const int vs = st & 127;
-        load_piece<F32>(R.vp, rv, (uint32_t)((vs >> 1) * v_row + ((int64_t)h * dv + j0 + (vs & 1) * 8) * ES));
-        const rsrc_t rg = make_rsrc(p.g + t0 * H, rows * H * 4);
-        R.g = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rg, (uint32_t)((lane * H + h) * 4), 0, 0));
+        if constexpr (TABLES) {
+            // V slice (lane l: rows l/2 and 32 + l/2, columns 8 (l%2)..+7)
+            // and the log-gates (lane t: token t) -- loaded by one wave only,
+            // so no two waves wait on the same cache lines
+            const rsrc_t rv = make_rsrc(static_cast<const char*>(p.v) + t0 * x.v_row, rows * x.v_row);
+            #pragma unroll
+            for (int i = 0; i < 2; ++i)
+                load_piece<F32>(R.vp[i], rv, (uint32_t)(((lane >> 1) + 32 * i) * x.v_row +
+                                                        ((int64_t)h * dv + j0 + 8 * (lane & 1)) * ES));
+            const rsrc_t rg = make_rsrc(p.g + t0 * H, rows * H * 4);
+            R.g = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rg, (uint32_t)((lane * H + h) * 4), 0, 0));
+        }
     };
 
-    auto store_chunk = [&](const St& R, int b) {
+    // K rows of a chunk into LDS; the gate wave also V, V w and the decay tables.
+    auto stage = [&](St& R, int bk, int bq) {
         #pragma unroll
         for (int u = 0; u < PK; ++u) {
             const int pc = st + NS_T * u;
@@ -286,273 +315,398 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
             const int d0 = (pc % (DK / 8)) * 8;
             bf16x8 hi, lo;
             split_piece<F32>(R.kp[u], hi, lo);
-            *reinterpret_cast<bf16x8*>(&sm.k[b][0][m * KP + d0]) = hi;
-            if (F32) *reinterpret_cast<bf16x8*>(&sm.k[b][NL - 1][m * KP + d0]) = lo;
+            *reinterpret_cast<bf16x8*>(&sm.k[bk][0][m * KP + d0]) = hi;
+                if (F32) *reinterpret_cast<bf16x8*>(&sm.k[bk][NL - 1][m * KP + d0]) = lo;
         }
-        // every state wave scans the chunk's log-gates: lane t holds G_t
-        const float x = wave_inclusive_sum(R.g);
-        const float glast = lane_value(x, 63);
-        const float wl = __expf(glast - x);  // w_t = exp(G_last - G_t)
-        const int vs = st & 127;
-        const float wm = __shfl(wl, vs >> 1, 64);
-        if (wave < 6) {  // V rows: raw (hi, lo) and V w (hi, lo)
-            const int m = vs >> 1;
-            const int jj = (vs & 1) * 8;
-            float f[8];
-            piece_f32<F32>(R.vp, f);
-            bf16x8 hi, lo;
-            split_piece<F32>(R.vp, hi, lo);
-            *reinterpret_cast<bf16x8*>(&sm.v[b][0][m * VP + jj]) = hi;
-            if (F32) *reinterpret_cast<bf16x8*>(&sm.v[b][NL - 1][m * VP + jj]) = lo;
+        if constexpr (TABLES) {
+            // the gate wave scans the chunk's log-gates (lane t holds G_t),
+            // stages V and V w (lane l: rows l/2 and 32 + l/2, columns
+            // 8 (l%2)..+7) and writes the decay tables
+            const float xs = wave_inclusive_sum(R.g);
+            const float glast = lane_value(xs, 63);
+            const float wl = __expf(glast - xs);  // w_t = exp(G_last - G_t)
             #pragma unroll
-            for (int e = 0; e < 8; ++e) f[e] *= wm;
-            split8(f, hi, lo);
-            *reinterpret_cast<bf16x8*>(&sm.vw[b][0][m * VP + jj]) = hi;
-            *reinterpret_cast<bf16x8*>(&sm.vw[b][1][m * VP + jj]) = lo;
-        }
-        if (wave == 4) {  // decay tables
+            for (int i = 0; i < 2; ++i) {
+                const int m = (lane >> 1) + 32 * i;
+                const int jj = 8 * (lane & 1);
+                const float wm = __shfl(wl, m, 64);
+                float f[8];
+                piece_f32<F32>(R.vp[i], f);
+                bf16x8 hi, lo;
+                split_piece<F32>(R.vp[i], hi, lo);
+                *reinterpret_cast<bf16x8*>(&sm.v[bq][0][m * VP + jj]) = hi;
+                if (F32) *reinterpret_cast<bf16x8*>(&sm.v[bq][NL - 1][m * VP + jj]) = lo;
+                #pragma unroll
+                for (int e = 0; e < 8; ++e) f[e] *= wm;
+                split_n<8>(f, hi, lo);
+                *reinterpret_cast<bf16x8*>(&sm.vw[bk][0][m * VP + jj]) = hi;
+                *reinterpret_cast<bf16x8*>(&sm.vw[bk][1][m * VP + jj]) = lo;
+            }
             float ge[4];
             #pragma unroll
-            for (int M = 0; M < 4; ++M) ge[M] = lane_value(x, 16 * M + 15);
+            for (int M = 0; M < 4; ++M) ge[M] = lane_value(xs, 16 * M + 15);
             const int blk = lane >> 4;
-            sm.G2[b][lane] = x * LOG2E;
-            sm.eG[b][lane] = __expf(x);
-            sm.bm[b][lane] = __expf(ge[blk] - x);
+            sm.G2[bq][lane] = xs * LOG2E;
+            sm.eG[bq][lane] = __expf(xs);
+            sm.bm[bq][lane] = __expf(ge[blk] - xs);
             f32x4 a;
             #pragma unroll
-            for (int M = 0; M < 4; ++M) a[M] = (M < blk) ? __expf(x - ge[M]) : 0.0f;
-            *reinterpret_cast<f32x4*>(&sm.ai[b][lane][0]) = a;
+            for (int M = 0; M < 4; ++M) a[M] = (M < blk) ? __expf(xs - ge[M]) : 0.0f;
+            *reinterpret_cast<f32x4*>(&sm.ai[bq][lane][0]) = a;
         }
     };
 
-    // S_j split into bf16 hi/lo planes [d][j] for the next chunk's X^T.
-    auto publish_state = [&](int b) {
+    // D = K^T (V w) over this wave's tiles of d, from zero
+    auto fold_delta = [&](int bk, f32x4 (&D)[NDW]) {
         #pragma unroll
-        for (int u = 0; u < NDW; ++u) {
-            const int d = (wq * NDW + u) * 16 + li;
-            bf16x4 hi, lo;
-            #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const __bf16 x = (__bf16)S[u][r];
-                hi[r] = x;
-                lo[r] = (__bf16)(S[u][r] - (float)x);
-            }
-            *reinterpret_cast<bf16x4*>(&sm.s[b][0][d * VP + 4 * grp]) = hi;
-            *reinterpret_cast<bf16x4*>(&sm.s[b][1][d * VP + 4 * grp]) = lo;
-        }
-    };
-
-    // S^T = exp(G_last) S^T + (V w)^T K over this wave's tiles
-    auto fold = [&](int b) {
-        const float decay = sm.eG[b][CH - 1];
-        #pragma unroll
-        for (int u = 0; u < NDW; ++u) {
-            #pragma unroll
-            for (int r = 0; r < 4; ++r) S[u][r] *= decay;
-        }
+        for (int u = 0; u < NDW; ++u) D[u] = f32x4{0.f, 0.f, 0.f, 0.f};
         #pragma unroll
         for (int mm = 0; mm < 2; ++mm) {
             const int m0 = 32 * mm + 8 * grp;
-            const bf16x8 wh = cat(tr4(sm.vw[b][0], VP, m0, 0, li), tr4(sm.vw[b][0], VP, m0 + 4, 0, li));
-            const bf16x8 wlo = cat(tr4(sm.vw[b][1], VP, m0, 0, li), tr4(sm.vw[b][1], VP, m0 + 4, 0, li));
+            const bf16x8 wh = cat(tr4(sm.vw[bk][0], VP, m0, 0, li), tr4(sm.vw[bk][0], VP, m0 + 4, 0, li));
+            const bf16x8 wlo = cat(tr4(sm.vw[bk][1], VP, m0, 0, li), tr4(sm.vw[bk][1], VP, m0 + 4, 0, li));
             #pragma unroll
             for (int u = 0; u < NDW; ++u) {
                 const int n0 = (wq * NDW + u) * 16;
-                const bf16x8 kh = cat(tr4(sm.k[b][0], KP, m0, n0, li), tr4(sm.k[b][0], KP, m0 + 4, n0, li));
-                S[u] = mma(wh, kh, S[u]);
-                S[u] = mma(wlo, kh, S[u]);
+                const bf16x8 kh = cat(tr4(sm.k[bk][0], KP, m0, n0, li), tr4(sm.k[bk][0], KP, m0 + 4, n0, li));
+                D[u] = mma(kh, wh, D[u]);
+                D[u] = mma(kh, wlo, D[u]);
                 if (F32) {
-                    const bf16x8 kl = cat(tr4(sm.k[b][NL - 1], KP, m0, n0, li),
-                                          tr4(sm.k[b][NL - 1], KP, m0 + 4, n0, li));
-                    S[u] = mma(wh, kl, S[u]);
+                    const bf16x8 kl = cat(tr4(sm.k[bk][NL - 1], KP, m0, n0, li),
+                                          tr4(sm.k[bk][NL - 1], KP, m0 + 4, n0, li));
+                    D[u] = mma(kl, wh, D[u]);
                 }
             }
         }
     };
 
-    // --------------------------------------------------------- output role
-    using QS = QStage<F32, NKK>;
-    // this output wave's 16 rows of Q for chunk c, straight into registers
-    auto load_q = [&](QS& Q, int64_t c) {
+    // S split into bf16 hi/lo planes of S^T [j][d] for the output waves' X
+    auto publish = [&](int bs) {
+        #pragma unroll
+        for (int u = 0; u < NDW; ++u) {
+            const int d0 = (wq * NDW + u) * 16 + 4 * grp;
+            float f[4] = {S[u][0], S[u][1], S[u][2], S[u][3]};
+            bf16x4 hi, lo;
+            split_n<4>(f, hi, lo);
+            *reinterpret_cast<bf16x4*>(&sm.s[bs][0][li * SP + d0]) = hi;
+            *reinterpret_cast<bf16x4*>(&sm.s[bs][1][li * SP + d0]) = lo;
+        }
+    };
+
+    // Cooperative L2 prefetch.  The 16-column slices of a head all read the
+    // head's full Q and K rows and share the 128-byte lines of V; fetched
+    // at the same moment by every slice, each line costs every workgroup a
+    // full HBM latency.  So the gate wave of each slice touches its eighth
+    // of the head's lines PREFETCH chunks ahead of the regular loads (rows
+    // 8 s + i/2 of Q and K, line i%2; rows 16 (s%4) + i of V, line s/4), and
+    // the other slices' loads then hit in L2.  The fetched value is only
+    // consumed (as an asm operand, forcing nothing but the load's wait) two
+    // steps later.
+    constexpr int PREFETCH = 6;
+    uint32_t pf[2] = {0u, 0u};
+    auto prefetch = [&](int slot, int64_t c) {
+        __asm__ volatile("" : : "v"(pf[slot]));
         const int64_t t0 = c * CH;
-        const rsrc_t rq = make_rsrc(static_cast<const char*>(p.q) + t0 * qk_row, (T - t0) * qk_row);
-        #pragma unroll
-        for (int kk = 0; kk < NKK; ++kk)
-            load_piece<F32>(Q.qp[kk], rq, (uint32_t)((16 * wq + li) * qk_row + ((int64_t)h * DK + 32 * kk + 8 * grp) * ES));
+        const int64_t rows = x.T - t0;
+        const int s8 = (j0 / DVS) & 7;
+        const int tsel = lane >> 4, i = lane & 15;
+        const uint32_t qoff = (uint32_t)((8 * s8 + (i >> 1)) * x.qk_row + (int64_t)h * DK * ES + (i & 1) * 128);
+        const uint32_t voff = (uint32_t)((16 * (s8 & 3) + i) * x.v_row + (int64_t)h * dv * ES + (s8 >> 2) * 128);
+        const int64_t row_b = tsel == 2 ? x.v_row : x.qk_row;
+        const void* base = tsel == 0 ? p.q : tsel == 1 ? p.k : p.v;
+        const rsrc_t r = make_rsrc(static_cast<const char*>(base) + t0 * row_b, tsel == 3 ? 0 : rows * row_b);
+        pf[slot] = __builtin_amdgcn_raw_buffer_load_b32(r, tsel == 2 ? voff : qoff, 0, 0);
     };
 
-    auto outputs = [&](int b, int64_t c, const QS& Q) {
-        const int w = wq;
-        const int i_row = 16 * w + li;
-        bf16x8 qh[NKK], ql[NKK];
-        #pragma unroll
-        for (int kk = 0; kk < NKK; ++kk) split_piece<F32>(Q.qp[kk], qh[kk], ql[kk]);
-        // A^T = K Q^T for the causal m-blocks mb <= w (uniform branch); lane
-        // (li, grp) of tile mb holds A^T[m = 16 mb + 4 grp + r][i = 16 w + li]
-        f32x4 at[4];
-        #pragma unroll
-        for (int mb = 0; mb < 4; ++mb) {
-            at[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
-            if (mb <= w) {
-                bf16x8 a[NKK], al[NKK];
-                #pragma unroll
-                for (int kk = 0; kk < NKK; ++kk) {
-                    const int off = (mb * 16 + li) * KP + 32 * kk + 8 * grp;
-                    a[kk] = *reinterpret_cast<const bf16x8*>(&sm.k[b][0][off]);
-                    if (F32) al[kk] = *reinterpret_cast<const bf16x8*>(&sm.k[b][NL - 1][off]);
-                }
-                #pragma unroll
-                for (int kk = 0; kk < NKK; ++kk) {
-                    at[mb] = mma(a[kk], qh[kk], at[mb]);
-                    if (F32) {
-                        at[mb] = mma(a[kk], ql[kk], at[mb]);
-                        at[mb] = mma(al[kk], qh[kk], at[mb]);
-                    }
-                }
-            }
-        }
-        // decay: factored tables below the diagonal tile, exp2 on it
+    // step c: loads of c+4, staging of c+2, D_{c+1}; S_c out; S_{c+1} in
+    auto step = [&](int64_t c, int u, St& Rc, St& Rs, f32x4 (&Dn)[NDW], const f32x4 (&Dc)[NDW]) {
+        if constexpr (TABLES) prefetch(u & 1, c + PREFETCH);
+        load_chunk(Rc, c + 4);
+        stage(Rs, u & 1, (u + 2) & 3);
+        fold_delta((u + 1) & 1, Dn);
+        const bool live = c < x.n;
         {
-            const f32x4 ai = *reinterpret_cast<const f32x4*>(&sm.ai[b][i_row][0]);
+            const bool on = live && p.chunk_states != nullptr;
+            const rsrc_t rc = make_rsrc(p.chunk_states + (on ? c * (int64_t)H * DK * dv : 0),
+                                        on ? (int64_t)H * DK * dv * 4 : 0);
             #pragma unroll
-            for (int mb = 0; mb < 4; ++mb) {
-                if (mb < w) {
-                    const f32x4 bmv = *reinterpret_cast<const f32x4*>(&sm.bm[b][mb * 16 + 4 * grp]);
-                    #pragma unroll
-                    for (int r = 0; r < 4; ++r) at[mb][r] = (at[mb][r] * ai[mb]) * bmv[r];
-                } else if (mb == w) {
-                    const float gi = sm.G2[b][i_row];
-                    const f32x4 gm = *reinterpret_cast<const f32x4*>(&sm.G2[b][mb * 16 + 4 * grp]);
-                    #pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const float pv = at[mb][r] * __builtin_amdgcn_exp2f(gi - gm[r]);
-                        at[mb][r] = (4 * grp + r <= li) ? pv : 0.0f;
-                    }
-                }
-            }
-        }
-        // O^T = V^T P^T, two m-blocks per MFMA; lane (li, grp) ends with
-        // O[i = 16 w + li][j0 + 4 grp + r]
-        f32x4 acc_o = {0.f, 0.f, 0.f, 0.f};
-        #pragma unroll
-        for (int pr = 0; pr < 2; ++pr) {
-            if (2 * pr <= w) {
-                float f[8];
+            for (int t = 0; t < NDW; ++t) {
                 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    f[r] = at[2 * pr][r];
-                    f[4 + r] = at[2 * pr + 1][r];
-                }
-                bf16x8 ph, pl;
-                split8(f, ph, pl);
-                const bf16x8 vh = cat(tr4(sm.v[b][0], VP, (2 * pr) * 16 + 4 * grp, 0, li),
-                                      tr4(sm.v[b][0], VP, (2 * pr + 1) * 16 + 4 * grp, 0, li));
-                acc_o = mma(vh, ph, acc_o);
-                acc_o = mma(vh, pl, acc_o);
-                if (F32) {
-                    const bf16x8 vl = cat(tr4(sm.v[b][NL - 1], VP, (2 * pr) * 16 + 4 * grp, 0, li),
-                                          tr4(sm.v[b][NL - 1], VP, (2 * pr + 1) * 16 + 4 * grp, 0, li));
-                    acc_o = mma(vl, ph, acc_o);
+                    const float sv = S[t][r];  // (a bit_cast of the vector element itself reads element 0)
+                    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, sv), rc,
+                                                          (uint32_t)(srow(t, r) * 4), 0, 0);
                 }
             }
         }
-        // X^T = S_j^T Q^T from the published S planes, hi and lo products in
-        // two independent accumulators
+        if (live) {
+            const float gamma = sm.eG[u][CH - 1];  // exp(G_last) of chunk c
+            #pragma unroll
+            for (int t = 0; t < NDW; ++t) {
+                #pragma unroll
+                for (int r = 0; r < 4; ++r) S[t][r] = __builtin_fmaf(gamma, S[t][r], Dc[t][r]);
+            }
+        }
+        publish((u + 1) & 1);
+        if (live) lds_barrier();
+    };
+
+    St R0, R1, R2, R3;
+    load_chunk(R0, 0);
+    load_chunk(R1, 1);
+    load_chunk(R2, 2);
+    load_chunk(R3, 3);
+    stage(R0, 0, 0);
+    stage(R1, 1, 1);
+    publish(0);
+    lds_barrier();
+    fold_delta(0, D0);
+    lds_barrier();
+    for (int64_t c = 0; c < x.n; c += 4) {
+        step(c, 0, R0, R2, D1, D0);
+        step(c + 1, 1, R1, R3, D0, D1);
+        step(c + 2, 2, R2, R0, D1, D0);
+        step(c + 3, 3, R3, R1, D0, D1);
+    }
+    if (p.final_state) {
+        #pragma unroll
+        for (int u = 0; u < NDW; ++u) {
+            #pragma unroll
+            for (int r = 0; r < 4; ++r) p.final_state[srow(u, r)] = S[u][r];
+        }
+    }
+    if constexpr (TABLES) __asm__ volatile("" : : "v"(pf[0]), "v"(pf[1]));
+}
+
+// ------------------------------------------------------------ output role
+// Output wave W owns rows i = 16 W + li of every chunk.
+template <int DK, bool F32, int W>
+__device__ __forceinline__ void output_role(const ScanParams& p, Smem<DK, F32>& sm, const Ctx& x) {
+    using S_ = Smem<DK, F32>;
+    constexpr int KP = S_::KP;
+    constexpr int SP = S_::SP;
+    constexpr int NL = S_::NL;
+    constexpr int ES = F32 ? 4 : 2;
+    constexpr int NKK = DK / 32;  // k-steps of 32 over dk
+    constexpr int PPR = DK * ES / 16;  // 16-byte pieces per Q row
+    constexpr int RPI = 64 / PPR;      // Q rows per coalesced load
+    constexpr int NQI = 16 / RPI;      // coalesced loads per 16 rows
+    constexpr int EPP = 16 / ES;       // elements per piece
+    using QS = QStage<NQI>;
+    struct QOp {                       // Q rows as MFMA operands (hi, lo)
+        bf16x8 h[NKK], l[NKK];
+    };
+    const int lane = x.lane, li = x.li, grp = x.grp, h = x.h, j0 = x.j0, dv = x.dv;
+    const int i_row = 16 * W + li;
+
+    // this wave's 16 rows of Q for chunk c, coalesced: load i, lane l reads
+    // piece l % PPR of row RPI i + l / PPR
+    auto load_q = [&](QS& Q, int64_t c) {
+        const int64_t t0 = c * CH;
+        const rsrc_t rq = make_rsrc(static_cast<const char*>(p.q) + t0 * x.qk_row, (x.T - t0) * x.qk_row);
+        #pragma unroll
+        for (int i = 0; i < NQI; ++i)
+            Q.qp[i] = __builtin_amdgcn_raw_buffer_load_b128(
+                rq, (uint32_t)((16 * W + RPI * i + lane / PPR) * x.qk_row + (int64_t)h * DK * ES + (lane % PPR) * 16), 0, 0);
+    };
+
+    // through this wave's own LDS rows into operand layout (lane (li, grp)
+    // gets row li, elements 32 kk + 8 grp..+7); the wave reads back only
+    // what it wrote, so no barrier is involved
+    auto q_operands = [&](const QS& Q, QOp& op) {
+        #pragma unroll
+        for (int i = 0; i < NQI; ++i) {
+            const int row = RPI * i + lane / PPR;
+            const int e0 = (lane % PPR) * EPP;
+            if constexpr (F32) {
+                const f32x4 a = __builtin_bit_cast(f32x4, Q.qp[i]);
+                float f[4] = {a[0], a[1], a[2], a[3]};
+                bf16x4 hi, lo;
+                split_n<4>(f, hi, lo);
+                *reinterpret_cast<bf16x4*>(&sm.q[W][0][row * SP + e0]) = hi;
+                *reinterpret_cast<bf16x4*>(&sm.q[W][NL - 1][row * SP + e0]) = lo;
+            } else {
+                *reinterpret_cast<u32x4*>(&sm.q[W][0][row * SP + e0]) = Q.qp[i];
+            }
+        }
+        #pragma unroll
+        for (int kk = 0; kk < NKK; ++kk) {
+            op.h[kk] = *reinterpret_cast<const bf16x8*>(&sm.q[W][0][li * SP + 32 * kk + 8 * grp]);
+            op.l[kk] = F32 ? *reinterpret_cast<const bf16x8*>(&sm.q[W][NL - 1][li * SP + 32 * kk + 8 * grp]) : bf16x8{};
+        }
+    };
+
+    // A^T = K Q^T for the causal m-blocks mb <= W; lane (li, grp) of tile mb
+    // holds A^T[m = 16 mb + 4 grp + r][i = 16 W + li]
+    auto scores = [&](const QOp& qo, int bk, f32x4 (&at)[4]) {
+        const bf16x8* qh = qo.h;
+        const bf16x8* ql = qo.l;
+        #pragma unroll
+        for (int mb = 0; mb <= W; ++mb) {
+            bf16x8 a[NKK], al[NKK];
+            #pragma unroll
+            for (int kk = 0; kk < NKK; ++kk) {
+                const int off = (mb * 16 + li) * KP + 32 * kk + 8 * grp;
+                a[kk] = *reinterpret_cast<const bf16x8*>(&sm.k[bk][0][off]);
+                if (F32) al[kk] = *reinterpret_cast<const bf16x8*>(&sm.k[bk][NL - 1][off]);
+            }
+            at[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+            #pragma unroll
+            for (int kk = 0; kk < NKK; ++kk) {
+                at[mb] = mma(a[kk], qh[kk], at[mb]);
+                if (F32) {
+                    at[mb] = mma(a[kk], ql[kk], at[mb]);
+                    at[mb] = mma(al[kk], qh[kk], at[mb]);
+                }
+            }
+        }
+    };
+
+    // decay, O^T = V^T P^T, X^T = S_c^T Q^T and the o store of chunk c
+    auto finish = [&](int64_t c, int u, const QOp& qo, f32x4 (&at)[4]) {
+        const bf16x8* qh = qo.h;
+        const bf16x8* ql = qo.l;
+        // decay: factored tables below the diagonal tile, exp2 on it
+        {
+            const f32x4 ai = *reinterpret_cast<const f32x4*>(&sm.ai[u][i_row][0]);
+            #pragma unroll
+            for (int mb = 0; mb < W; ++mb) {
+                const f32x4 bmv = *reinterpret_cast<const f32x4*>(&sm.bm[u][mb * 16 + 4 * grp]);
+                #pragma unroll
+                for (int r = 0; r < 4; ++r) at[mb][r] = (at[mb][r] * ai[mb]) * bmv[r];
+            }
+            const float gi = sm.G2[u][i_row];
+            const f32x4 gm = *reinterpret_cast<const f32x4*>(&sm.G2[u][W * 16 + 4 * grp]);
+            #pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const float pv = at[W][r] * __builtin_amdgcn_exp2f(gi - gm[r]);
+                at[W][r] = (4 * grp + r <= li) ? pv : 0.0f;
+            }
+        }
+        // O = P V, two m-blocks per MFMA (the score accumulators are P in
+        // A-operand layout); lane (li, grp) ends with O[i = 16 W + 4 grp + r][j0 + li]
+        f32x4 acc_o = {0.f, 0.f, 0.f, 0.f};
+        #pragma unroll
+        for (int pr = 0; 2 * pr <= W; ++pr) {
+            float f[8];
+            #pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                f[r] = at[2 * pr][r];
+                f[4 + r] = (2 * pr + 1 <= W) ? at[2 * pr + 1][r] : 0.0f;
+            }
+            bf16x8 ph, pl;
+            split_n<8>(f, ph, pl);
+            const bf16x8 vh = cat(tr4(sm.v[u][0], VP, (2 * pr) * 16 + 4 * grp, 0, li),
+                                  tr4(sm.v[u][0], VP, (2 * pr + 1) * 16 + 4 * grp, 0, li));
+            acc_o = mma(ph, vh, acc_o);
+            acc_o = mma(pl, vh, acc_o);
+            if (F32) {
+                const bf16x8 vl = cat(tr4(sm.v[u][NL - 1], VP, (2 * pr) * 16 + 4 * grp, 0, li),
+                                      tr4(sm.v[u][NL - 1], VP, (2 * pr + 1) * 16 + 4 * grp, 0, li));
+                acc_o = mma(ph, vl, acc_o);
+            }
+        }
+        // X = Q S_c from the published S^T planes, hi and lo products in two
+        // independent accumulators
         f32x4 acc_x = {0.f, 0.f, 0.f, 0.f}, acc_xl = {0.f, 0.f, 0.f, 0.f};
         {
+            const int bs = u & 1;
             bf16x8 sh[NKK], sl[NKK];
             #pragma unroll
             for (int kk = 0; kk < NKK; ++kk) {
-                const int k0 = 32 * kk + 8 * grp;
-                sh[kk] = cat(tr4(sm.s[b][0], VP, k0, 0, li), tr4(sm.s[b][0], VP, k0 + 4, 0, li));
-                sl[kk] = cat(tr4(sm.s[b][1], VP, k0, 0, li), tr4(sm.s[b][1], VP, k0 + 4, 0, li));
+                const int off = li * SP + 32 * kk + 8 * grp;
+                sh[kk] = *reinterpret_cast<const bf16x8*>(&sm.s[bs][0][off]);
+                sl[kk] = *reinterpret_cast<const bf16x8*>(&sm.s[bs][1][off]);
             }
             #pragma unroll
             for (int kk = 0; kk < NKK; ++kk) {
-                acc_x = mma(sh[kk], qh[kk], acc_x);
-                acc_xl = mma(sl[kk], qh[kk], acc_xl);
-                if (F32) acc_xl = mma(sh[kk], ql[kk], acc_xl);
+                acc_x = mma(qh[kk], sh[kk], acc_x);
+                acc_xl = mma(qh[kk], sl[kk], acc_xl);
+                if (F32) acc_xl = mma(ql[kk], sh[kk], acc_xl);
             }
             acc_x += acc_xl;
         }
-        // o row i = 16 w + li, columns j0 + 4 grp .. + 3: one 16-byte store;
-        // rows past T fall outside the chunk's buffer range and are dropped
+        // o rows i = 16 W + 4 grp + r, column j0 + li: for each r the 16
+        // lanes of a group store 64 contiguous bytes; rows past T fall outside
+        // the chunk's buffer range and are dropped
         {
             const int64_t t0 = c * CH;
-            const rsrc_t ro = make_rsrc(reinterpret_cast<const char*>(p.o) + t0 * o_row, (T - t0) * o_row);
-            const float eg = sm.eG[b][i_row];
-            f32x4 val;
+            const rsrc_t ro = make_rsrc(reinterpret_cast<const char*>(p.o) + t0 * x.o_row, (x.T - t0) * x.o_row);
+            const f32x4 eg = *reinterpret_cast<const f32x4*>(&sm.eG[u][16 * W + 4 * grp]);
             #pragma unroll
-            for (int r = 0; r < 4; ++r) val[r] = p.scale * (eg * acc_x[r] + acc_o[r]);
-            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, val), ro,
-                                                   (uint32_t)(i_row * o_row + ((int64_t)h * dv + j0 + 4 * grp) * 4), 0, 0);
+            for (int r = 0; r < 4; ++r) {
+                const float val = p.scale * (eg[r] * acc_x[r] + acc_o[r]);
+                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, val), ro,
+                                                      (uint32_t)((16 * W + 4 * grp + r) * x.o_row + ((int64_t)h * dv + j0 + li) * 4),
+                                                      0, 0);
+            }
         }
     };
 
-    // One loop per role; both run the same number of barriers.  The loops
-    // advance two chunks per iteration so that the two register stages swap
-    // roles without copies; a chunk index past the end does no visible work.
-    // One loop per role; both run one barrier per chunk.  Each loop advances
-    // three chunks per iteration so that three register stages rotate
-    // without copies (loads run three chunks ahead); a chunk index past the
-    // end issues only empty-range memory accesses and skips the barrier.
-    if (state_role) {
-        auto state_step = [&](int64_t c, St& Rfree, const St& Rnext) {
-            const int b = (int)(c & 1);
-            load_chunk(Rfree, c + 3);
-            if (c + 1 < n_chunks) store_chunk(Rnext, b ^ 1);
-            {
-                const bool live = c < n_chunks && p.chunk_states != nullptr;
-                const rsrc_t rc = make_rsrc(p.chunk_states + (live ? c : 0) * (int64_t)H * DK * dv,
-                                            live ? (int64_t)H * DK * dv * 4 : 0);
-                #pragma unroll
-                for (int u = 0; u < NDW; ++u) {
-                    const int d = (wq * NDW + u) * 16 + li;
-                    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, S[u]), rc,
-                                                           (uint32_t)((((int64_t)h * DK + d) * dv + j0 + 4 * grp) * 4), 0, 0);
-                }
-            }
-            if (c < n_chunks) {
-                fold(b);
-                publish_state(b ^ 1);
-                lds_barrier();
-            }
-        };
-        St R0, R1, R2;
-        load_chunk(R0, 0);
-        load_chunk(R1, 1);
-        load_chunk(R2, 2);
-        store_chunk(R0, 0);
-        publish_state(0);
-        lds_barrier();
-        for (int64_t c = 0; c < n_chunks; c += 3) {
-            state_step(c, R0, R1);
-            state_step(c + 1, R1, R2);
-            state_step(c + 2, R2, R0);
-        }
-        if (p.final_state) {
-            #pragma unroll
-            for (int u = 0; u < NDW; ++u) {
-                const int d = (wq * NDW + u) * 16 + li;
-                *reinterpret_cast<f32x4*>(p.final_state + ((int64_t)h * DK + d) * dv + j0 + 4 * grp) = S[u];
-            }
-        }
-    } else {
-        auto out_step = [&](int64_t c, QS& Q) {
-            outputs((int)(c & 1), c, Q);  // past the end: reads stale LDS, stores nothing
-            load_q(Q, c + 3);
-            if (c < n_chunks) lds_barrier();
-        };
-        QS Q0, Q1, Q2;
-        load_q(Q0, 0);
-        load_q(Q1, 1);
-        load_q(Q2, 2);
-        lds_barrier();
-        for (int64_t c = 0; c < n_chunks; c += 3) {
-            out_step(c, Q0);
-            out_step(c + 1, Q1);
-            out_step(c + 2, Q2);
-        }
+    // step c: Q operands and scores of chunk c+1, the rest of chunk c, then
+    // the loads of Q for chunk c+4 into the freed register stage
+    auto step = [&](int64_t c, int u, QS& Qc, const QS& Qn, const QOp& oc, QOp& on, f32x4 (&atc)[4],
+                    f32x4 (&atn)[4]) {
+        q_operands(Qn, on);
+        scores(on, (u + 1) & 1, atn);
+        finish(c, u, oc, atc);
+        load_q(Qc, c + 4);
+        if (c < x.n) lds_barrier();
+    };
+
+    QS Q0, Q1, Q2, Q3;
+    QOp O0, O1;
+    f32x4 A0[4], A1[4];
+    load_q(Q0, 0);
+    load_q(Q1, 1);
+    load_q(Q2, 2);
+    load_q(Q3, 3);
+    lds_barrier();
+    q_operands(Q0, O0);
+    scores(O0, 0, A0);
+    lds_barrier();
+    for (int64_t c = 0; c < x.n; c += 4) {
+        step(c, 0, Q0, Q1, O0, O1, A0, A1);
+        step(c + 1, 1, Q1, Q2, O1, O0, A1, A0);
+        step(c + 2, 2, Q2, Q3, O0, O1, A0, A1);
+        step(c + 3, 3, Q3, Q0, O1, O0, A1, A0);
+    }
+}
+
+template <int DK, bool F32>
+__global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
+    __shared__ Smem<DK, F32> sm;
+    const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform
+
+    // workgroup -> (head, slice); slices of one head share an XCD (and its L2)
+    // when the grid allows it (workgroups go round-robin over 8 XCDs).
+    Ctx x;
+    x.H = p.H;
+    x.dv = p.dv;
+    const int NS = x.dv / DVS;
+    const int N = x.H * NS;
+    int logical = blockIdx.x;
+    if ((N % 8) == 0 && ((N / 8) % NS) == 0) logical = (blockIdx.x % 8) * (N / 8) + blockIdx.x / 8;
+    x.h = logical / NS;
+    x.j0 = (logical % NS) * DVS;
+    x.lane = tid & 63;
+    x.li = x.lane & 15;
+    x.grp = x.lane >> 4;
+    x.T = p.T;
+    x.n = (p.T + CH - 1) / CH;
+    constexpr int ES = F32 ? 4 : 2;
+    x.qk_row = (int64_t)x.H * DK * ES;
+    x.v_row = (int64_t)x.H * x.dv * ES;
+    x.o_row = (int64_t)x.H * x.dv * 4;
+
+    switch (wave) {
+        case 0: output_role<DK, F32, 0>(p, sm, x); break;
+        case 1: output_role<DK, F32, 1>(p, sm, x); break;
+        case 2: output_role<DK, F32, 2>(p, sm, x); break;
+        case 3: output_role<DK, F32, 3>(p, sm, x); break;
+        case 4: state_role<DK, F32, true>(p, sm, x, 0); break;
+        default: state_role<DK, F32, false>(p, sm, x, wave - 4); break;
     }
 }
 
@@ -566,8 +720,8 @@ hipError_t launch_t(const ScanParams& p, hipStream_t stream) {
 }  // namespace
 
 hipError_t launch_linattn_scan(const ScanParams& p, hipStream_t stream) {
-    // fp32 inputs keep hi and lo planes of K, Q and V in LDS; at dk = 128 that
-    // exceeds the 160 KiB of LDS, so fp32 inputs are limited to dk = 64.
+    // fp32 inputs keep hi and lo planes of K and V in LDS; the scan supports
+    // them at dk = 64.
     if (p.dk == 128 && !p.in_f32) return launch_t<128, false>(p, stream);
     if (p.dk == 64) return p.in_f32 ? launch_t<64, true>(p, stream) : launch_t<64, false>(p, stream);
     return hipErrorInvalidValue;

@@ -41,11 +41,11 @@ MFMA_BF16_PEAK_TFS = 2500.0  # MI355X dense bf16 MFMA, TFLOP/s
 # unchanged.  Summary and commands: profiles/hybrid48_hbm_traffic.md.
 MEASURED_TRAFFIC = {
     "scan_cs": {"src": "paper_2606_20537_amd/csrc/linattn_scan.hip",
-                "sha256": "b5c413863e7aa55a87f62dfabb01486ced737b407ded8b16fbf99097c6a413a1",
-                "bytes": 1239916013},
+                "sha256": "6469e8dd13233581a7a272e8675453243621e36843d7ac473630a9739554b308",
+                "bytes": 1227799453},
     "restore": {"src": "paper_2606_20537_amd/csrc/capsule_copy.hip",
-                "sha256": "5bd781de8a324d6fa882746aa0aebf26163ee341032e6e2aba9db73093b0ed60",
-                "bytes": 1763913072},
+                "sha256": "7c114eda4a9bfbb8004abca49d610710b02b7f73425ed97266d767f35e4ffc66",
+                "bytes": 1763905201},
 }
 
 

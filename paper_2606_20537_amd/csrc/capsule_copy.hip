@@ -56,15 +56,16 @@ __device__ inline uint32_t last_le(const uint32_t* a, uint32_t n, uint32_t x) {
     return lo;
 }
 
-// kThreads threads of kUnroll 16-byte vectors each form one tile.
-template <int kThreads, int kUnroll, bool NT_LD, bool NT_ST>
+// kThreads threads of kUnroll 16-byte vectors each form one tile; kPtr
+// destination pointers (buffers x destination sets) fit in LDS.
+template <int kThreads, int kUnroll, bool NT_LD, bool NT_ST, int kPtr>
 __global__ __launch_bounds__(kThreads) void capsule_copy_kernel(const CopyParams p) {
     constexpr uint32_t kTileVec = (uint32_t)kThreads * kUnroll;
     constexpr int kPer = (kMaxSeg + 1 + kThreads - 1) / kThreads;  // table entries per thread
     __shared__ uint64_t s_start[kMaxSeg + 1];  // capsule vector offset of buffer i
     __shared__ uint32_t s_tile[kMaxSeg + 1];   // first tile of buffer i
     __shared__ uint32_t s_wave[kThreads / 64];
-    __shared__ uint64_t s_ptr[kMaxPtrLds];     // live pointers of the current rep
+    __shared__ uint64_t s_ptr[kPtr];           // live pointers of the current rep
 
     const uint32_t tid = threadIdx.x;
     const uint32_t lane = tid & 63, wave = tid >> 6;
@@ -185,13 +186,14 @@ __global__ __launch_bounds__(kThreads) void capsule_copy_kernel(const CopyParams
 
 }  // namespace
 
-template <int kThreads, int kUnroll, bool NT_LD, bool NT_ST>
+template <int kThreads, int kUnroll, bool NT_LD, bool NT_ST, int kPtr>
 hipError_t launch_t(const CopyParams& p, hipStream_t stream) {
     constexpr uint64_t kTileVec = (uint64_t)kThreads * kUnroll;
+    if (p.n_seg * p.n_dst > (uint32_t)kPtr) return hipErrorInvalidValue;
     // one block per tile; every buffer adds at most one partial tile
     const uint64_t tiles = (p.nvec / kTileVec + p.n_seg) * p.n_rep;
     if (tiles > 0x7fffffffull) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((capsule_copy_kernel<kThreads, kUnroll, NT_LD, NT_ST>), dim3((unsigned)tiles),
+    hipLaunchKernelGGL((capsule_copy_kernel<kThreads, kUnroll, NT_LD, NT_ST, kPtr>), dim3((unsigned)tiles),
                        dim3(kThreads), 0, stream, p);
     return hipGetLastError();
 }
@@ -207,9 +209,12 @@ hipError_t launch_copy(const CopyParams& p, int num_cus, hipStream_t stream) {
     //    512 threads, streamed;
     //  * gather-restore: 16 KiB tiles with cached loads, so that a gallery
     //    small enough for the 256 MB Infinity Cache stays there across resets.
-    if (p.n_dst > 1) return launch_t<512, 1, true, true>(p, stream);
-    if (p.n_rep > 1) return launch_t<256, 4, false, false>(p, stream);
-    return launch_t<256, 4, true, true>(p, stream);
+    // Only fork keeps several destination pointer tables in LDS; the other
+    // verbs size that table for one set, which leaves room for eight blocks
+    // per CU.
+    if (p.n_dst > 1) return launch_t<512, 1, true, true, kMaxPtrLds>(p, stream);
+    if (p.n_rep > 1) return launch_t<256, 4, false, false, kMaxSeg>(p, stream);
+    return launch_t<256, 4, true, true, kMaxSeg>(p, stream);
 }
 
 }  // namespace cap

@@ -402,7 +402,7 @@ __device__ __forceinline__ void state_role(const ScanParams& p, Smem<DK, F32>& s
     // the other slices' loads then hit in L2.  The fetched value is only
     // consumed (as an asm operand, forcing nothing but the load's wait) two
     // steps later.
-    constexpr int PREFETCH = 6;
+    constexpr int PREFETCH = 5;
     uint32_t pf[2] = {0u, 0u};
     auto prefetch = [&](int slot, int64_t c) {
         __asm__ volatile("" : : "v"(pf[slot]));

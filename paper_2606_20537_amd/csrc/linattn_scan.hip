@@ -248,10 +248,12 @@ struct Ctx {
 // read zeros, stores are dropped -- so the compiler's in-order memory
 // counters stay exact and the prefetch is never drained; a step past the end
 // changes no state, writes only LDS buffers no live step reads, and skips
-// the barrier.  Both roles run two barriers in the prologue and one per chunk.
+// the barrier.  Both roles run two barriers in the prologue and one per
+// chunk; a call of at most one chunk takes a straight-line path through the
+// same per-chunk code with a single barrier in both roles.
 
 // ------------------------------------------------------------- state role
-template <int DK, bool F32, bool TABLES>
+template <int DK, bool F32, bool ONE, bool TABLES>
 __device__ __forceinline__ void state_role(const ScanParams& p, Smem<DK, F32>& sm, const Ctx& x, int wq) {
     using S_ = Smem<DK, F32>;
     constexpr int KP = S_::KP;
@@ -418,6 +420,40 @@ __device__ __forceinline__ void state_role(const ScanParams& p, Smem<DK, F32>& s
         pf[slot] = __builtin_amdgcn_raw_buffer_load_b32(r, tsel == 2 ? voff : qoff, 0, 0);
     };
 
+    // S_c as chunk state c (an empty buffer range when not wanted)
+    auto store_state = [&](int64_t c, bool live) {
+        const bool on = live && p.chunk_states != nullptr;
+        const rsrc_t rc = make_rsrc(p.chunk_states + (on ? c * (int64_t)H * DK * dv : 0),
+                                    on ? (int64_t)H * DK * dv * 4 : 0);
+        #pragma unroll
+        for (int t = 0; t < NDW; ++t) {
+            #pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const float sv = S[t][r];  // (a bit_cast of the vector element itself reads element 0)
+                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, sv), rc,
+                                                      (uint32_t)(srow(t, r) * 4), 0, 0);
+            }
+        }
+    };
+    // S_{c+1} = exp(G_last of chunk c) S_c + D_c, tables of chunk c in buffer bq
+    auto advance = [&](int bq, const f32x4 (&Dc)[NDW]) {
+        const float gamma = sm.eG[bq][CH - 1];
+        #pragma unroll
+        for (int t = 0; t < NDW; ++t) {
+            #pragma unroll
+            for (int r = 0; r < 4; ++r) S[t][r] = __builtin_fmaf(gamma, S[t][r], Dc[t][r]);
+        }
+    };
+    auto store_final = [&]() {
+        if (p.final_state) {
+            #pragma unroll
+            for (int u = 0; u < NDW; ++u) {
+                #pragma unroll
+                for (int r = 0; r < 4; ++r) p.final_state[srow(u, r)] = S[u][r];
+            }
+        }
+    };
+
     // step c: loads of c+4, staging of c+2, D_{c+1}; S_c out; S_{c+1} in
     auto step = [&](int64_t c, int u, St& Rc, St& Rs, f32x4 (&Dn)[NDW], const f32x4 (&Dc)[NDW]) {
         if constexpr (TABLES) prefetch(u & 1, c + PREFETCH);
@@ -425,31 +461,28 @@ __device__ __forceinline__ void state_role(const ScanParams& p, Smem<DK, F32>& s
         stage(Rs, u & 1, (u + 2) & 3);
         fold_delta((u + 1) & 1, Dn);
         const bool live = c < x.n;
-        {
-            const bool on = live && p.chunk_states != nullptr;
-            const rsrc_t rc = make_rsrc(p.chunk_states + (on ? c * (int64_t)H * DK * dv : 0),
-                                        on ? (int64_t)H * DK * dv * 4 : 0);
-            #pragma unroll
-            for (int t = 0; t < NDW; ++t) {
-                #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const float sv = S[t][r];  // (a bit_cast of the vector element itself reads element 0)
-                    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, sv), rc,
-                                                          (uint32_t)(srow(t, r) * 4), 0, 0);
-                }
-            }
-        }
-        if (live) {
-            const float gamma = sm.eG[u][CH - 1];  // exp(G_last) of chunk c
-            #pragma unroll
-            for (int t = 0; t < NDW; ++t) {
-                #pragma unroll
-                for (int r = 0; r < 4; ++r) S[t][r] = __builtin_fmaf(gamma, S[t][r], Dc[t][r]);
-            }
-        }
+        store_state(c, live);
+        if (live) advance(u, Dc);
         publish((u + 1) & 1);
         if (live) lds_barrier();
     };
+
+    if constexpr (ONE) {
+        // At most one chunk (decode steps, short continuations): the same
+        // per-chunk arithmetic in straight line, one barrier.
+        St R0;
+        load_chunk(R0, 0);
+        stage(R0, 0, 0);
+        publish(0);
+        lds_barrier();
+        if (x.n == 1) {
+            fold_delta(0, D0);
+            store_state(0, true);
+            advance(0, D0);
+        }
+        store_final();
+        return;
+    } else {
 
     St R0, R1, R2, R3;
     load_chunk(R0, 0);
@@ -468,19 +501,14 @@ __device__ __forceinline__ void state_role(const ScanParams& p, Smem<DK, F32>& s
         step(c + 2, 2, R2, R0, D1, D0);
         step(c + 3, 3, R3, R1, D0, D1);
     }
-    if (p.final_state) {
-        #pragma unroll
-        for (int u = 0; u < NDW; ++u) {
-            #pragma unroll
-            for (int r = 0; r < 4; ++r) p.final_state[srow(u, r)] = S[u][r];
-        }
-    }
+    store_final();
     if constexpr (TABLES) __asm__ volatile("" : : "v"(pf[0]), "v"(pf[1]));
+    }
 }
 
 // ------------------------------------------------------------ output role
 // Output wave W owns rows i = 16 W + li of every chunk.
-template <int DK, bool F32, int W>
+template <int DK, bool F32, bool ONE, int W>
 __device__ __forceinline__ void output_role(const ScanParams& p, Smem<DK, F32>& sm, const Ctx& x) {
     using S_ = Smem<DK, F32>;
     constexpr int KP = S_::KP;
@@ -657,6 +685,16 @@ __device__ __forceinline__ void output_role(const ScanParams& p, Smem<DK, F32>& 
     QS Q0, Q1, Q2, Q3;
     QOp O0, O1;
     f32x4 A0[4], A1[4];
+    if constexpr (ONE) {  // at most one chunk: straight line, one barrier
+        load_q(Q0, 0);
+        lds_barrier();
+        if (x.n == 1) {
+            q_operands(Q0, O0);
+            scores(O0, 0, A0);
+            finish(0, 0, O0, A0);
+        }
+        return;
+    } else {
     load_q(Q0, 0);
     load_q(Q1, 1);
     load_q(Q2, 2);
@@ -671,9 +709,11 @@ __device__ __forceinline__ void output_role(const ScanParams& p, Smem<DK, F32>& 
         step(c + 2, 2, Q2, Q3, O0, O1, A0, A1);
         step(c + 3, 3, Q3, Q0, O1, O0, A1, A0);
     }
+    }
 }
 
-template <int DK, bool F32>
+// ONE: the call holds at most one chunk.
+template <int DK, bool F32, bool ONE>
 __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
     __shared__ Smem<DK, F32> sm;
     const int tid = threadIdx.x;
@@ -701,19 +741,20 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
     x.o_row = (int64_t)x.H * x.dv * 4;
 
     switch (wave) {
-        case 0: output_role<DK, F32, 0>(p, sm, x); break;
-        case 1: output_role<DK, F32, 1>(p, sm, x); break;
-        case 2: output_role<DK, F32, 2>(p, sm, x); break;
-        case 3: output_role<DK, F32, 3>(p, sm, x); break;
-        case 4: state_role<DK, F32, true>(p, sm, x, 0); break;
-        default: state_role<DK, F32, false>(p, sm, x, wave - 4); break;
+        case 0: output_role<DK, F32, ONE, 0>(p, sm, x); break;
+        case 1: output_role<DK, F32, ONE, 1>(p, sm, x); break;
+        case 2: output_role<DK, F32, ONE, 2>(p, sm, x); break;
+        case 3: output_role<DK, F32, ONE, 3>(p, sm, x); break;
+        case 4: state_role<DK, F32, ONE, true>(p, sm, x, 0); break;
+        default: state_role<DK, F32, ONE, false>(p, sm, x, wave - 4); break;
     }
 }
 
 template <int DK, bool F32>
 hipError_t launch_t(const ScanParams& p, hipStream_t stream) {
     const unsigned grid = (unsigned)(p.H * (p.dv / DVS));
-    hipLaunchKernelGGL((linattn_scan_kernel<DK, F32>), dim3(grid), dim3(NT), 0, stream, p);
+    if (p.T <= CH) hipLaunchKernelGGL((linattn_scan_kernel<DK, F32, true>), dim3(grid), dim3(NT), 0, stream, p);
+    else hipLaunchKernelGGL((linattn_scan_kernel<DK, F32, false>), dim3(grid), dim3(NT), 0, stream, p);
     return hipGetLastError();
 }
 

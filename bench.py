@@ -34,6 +34,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, GB/s
 MFMA_BF16_PEAK_TFS = 2500.0  # MI355X dense bf16 MFMA, TFLOP/s
+LINK_PEAK_GBS = 64.0         # host link, PCIe 5.0 x16, one direction
 
 # HBM bytes per launch from rocprofv3 FETCH_SIZE / WRITE_SIZE runs (FETCH_SIZE
 # scaled by 1.99954 from a plain copy of known size); the counters belong to
@@ -279,6 +280,29 @@ def main():
     ms = {k: float(np.mean([r[0][k][0].elapsed_time(r[0][k][1]) for r in recs])) for k in phases}
     ms_per_step = wall * 1e3 / args.steps
 
+    # ---- host tier, outside the timed step: demote the capsule to pinned
+    # host memory and promote it back (each a stream-ordered copy over the
+    # host link), one warm-up and three timed rounds, checked bitwise
+    c_dev = recs[-1][1][0]
+    h_arena = torch.empty(cap_bytes, dtype=torch.uint8, pin_memory=True)
+    d_arena = torch.empty(cap_bytes, dtype=torch.uint8, device=dev)
+    tier_ms = {"demote": [], "promote": []}
+    with torch.cuda.stream(stream):
+        for rnd in range(4):
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            e[0].record(stream)
+            c_host = cap.capsule_move(c_dev, h_arena, stream=stream)
+            e[1].record(stream)
+            c_back = cap.capsule_move(c_host, d_arena, stream=stream)
+            e[2].record(stream)
+            stream.synchronize()
+            if rnd:
+                tier_ms["demote"].append(e[0].elapsed_time(e[1]))
+                tier_ms["promote"].append(e[1].elapsed_time(e[2]))
+    assert cap.capsule_tier(c_host) == cap.CAP_TIER_HOST and cap.capsule_tier(c_back) == cap.CAP_TIER_DEVICE
+    assert torch.equal(d_arena, arena)
+    demote_ms, promote_ms = float(np.median(tier_ms["demote"])), float(np.median(tier_ms["promote"]))
+
     # post-run spot check: every fork branch holds the capsule's bytes (the
     # set starts with lin0.state; KV is not touched by the continuation)
     nst = H * dk * dv * 4
@@ -331,6 +355,12 @@ def main():
         "roofline_scan_final_only": {"bound": "hbm", "algorithmic_bytes_per_launch": scan_b_final,
                                      "achieved": round(scan_b_final / (ms["scan_final"] / n_lin * 1e-3) / 1e9, 2),
                                      "unit": "GB/s"},
+        "host_tier": {"bytes": cap_bytes, "demote_ms": round(demote_ms, 3), "promote_ms": round(promote_ms, 3),
+                      "demote_gbs": round(cap_bytes / (demote_ms * 1e-3) / 1e9, 2),
+                      "promote_gbs": round(cap_bytes / (promote_ms * 1e-3) / 1e9, 2),
+                      "link": "host link, PCIe 5.0 x16", "peak": LINK_PEAK_GBS, "unit": "GB/s",
+                      "promote_frac": round(cap_bytes / (promote_ms * 1e-3) / 1e9 / LINK_PEAK_GBS, 4),
+                      "capsule_ttft_ms_from_host": round(promote_ms + ms["restore"] + ms["continue"], 4)},
         "setup_s": round(t_setup, 1),
     }
     if not args.no_cpu_baseline:

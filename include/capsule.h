@@ -58,7 +58,8 @@ extern "C" {
 #define CAP_E_DIGEST       (-3)  /* prefix digest or deployment key mismatch           */
 #define CAP_E_UNSUPPORTED  (-4)  /* unknown buffer kind, unsupported shape or dtype    */
 #define CAP_E_ALIGN        (-5)  /* pointer or size not a multiple of 16 bytes         */
-#define CAP_E_STATE        (-6)  /* set position is not the aligned boundary           */
+#define CAP_E_STATE        (-6)  /* set position is not the aligned boundary, or the
+                                     capsule is not device-resident                   */
 #define CAP_E_HIP          (-7)  /* HIP runtime error (no device, allocation, launch)  */
 
 /* Static message for a status code (never NULL). */
@@ -76,6 +77,12 @@ CAP_API const char* cap_status_string(int status);
 
 #define CAP_DTYPE_F32  0
 #define CAP_DTYPE_BF16 1
+
+/* Capsule tiers (§3 Algorithm 1: snapshot returns a tiered handle; §4: the
+ * contract's one cross-space mechanism is host-backed buffers plus an
+ * asynchronous copy, so a capsule can be parked off the GPU). */
+#define CAP_TIER_DEVICE 0u  /* arena in the current device's memory              */
+#define CAP_TIER_HOST   1u  /* arena in page-locked host memory the device maps   */
 
 /* One named live buffer.  dptr: device pointer, 16-byte aligned, owned by the
  * caller.  row_bytes: multiple of 16, > 0.  rows: > 0.  reserved: 0. */
@@ -131,20 +138,25 @@ CAP_API int capsule_bytes(cap_set set, uint64_t P, uint64_t* bytes);
  * must equal P' (CAP_E_STATE otherwise -- the fixed buffers must hold the
  * state at P', e.g. from a prefill that stopped at P' or from the scan's
  * chunk-boundary state output); P' must fit every positional buffer
- * (CAP_E_SIZE).  Copies the set, valid at P', into `arena` (device,
- * caller-owned, 16-byte aligned, >= capsule_bytes, disjoint from every live
- * buffer) in one launch: buffers in set order, positional buffers
- * contributing rows [0, P'), fixed buffers all their bytes.  *out receives a
- * host header {P', prefix_digest, deploy key, layout}; the arena stays the
- * caller's and must outlive the header's use. */
+ * (CAP_E_SIZE).  Copies the set, valid at P', into `arena` (caller-owned,
+ * 16-byte aligned, >= capsule_bytes, disjoint from every live buffer) in one
+ * launch: buffers in set order, positional buffers contributing rows
+ * [0, P'), fixed buffers all their bytes.  The arena is memory of the
+ * current device (a device-tier capsule) or page-locked host memory from
+ * hipHostMalloc (a host-tier capsule, written across the host link); any
+ * other pointer is CAP_E_INVAL.  *out receives a host header {P',
+ * prefix_digest, deploy key, layout, tier}; the arena stays the caller's and
+ * must outlive the header's use. */
 CAP_API int capsule_snapshot(cap_set live, uint64_t P, uint64_t prefix_digest,
                              void* arena, uint64_t arena_bytes, void* stream,
                              cap_capsule* out);
 
 /* restore (§3 Algorithm 1; rollback is a restore of an earlier capsule):
  * checks, in order, the prefix digest and the set's deployment key
- * (CAP_E_DIGEST), then that the set's layout equals the capsule's
- * (CAP_E_SIZE); then copies the arena back into the live buffers in one
+ * (CAP_E_DIGEST), that the capsule is device-resident (CAP_E_STATE: a
+ * host-tier capsule is promoted first, with capsule_move), then that the
+ * set's layout equals the capsule's (CAP_E_SIZE); then copies the arena back
+ * into the live buffers in one
  * launch and rebinds the boundary: the set's position becomes P' (returned
  * in *P_restored, which may be NULL).  Positional rows at or beyond P' are
  * not written. */
@@ -173,6 +185,21 @@ CAP_API int capsule_gather_restore(const cap_capsule* gallery, uint32_t n_galler
 CAP_API int capsule_info(cap_capsule cap, uint64_t* P_aligned, uint64_t* bytes,
                          uint64_t* prefix_digest, uint64_t* deploy_key,
                          const void** arena);
+
+/* Promotion / demotion (§3 Algorithm 1: "if not GPU-resident, promote";
+ * §4: host-backed buffers plus cross-space asynchronous copy).  Copies the
+ * capsule's bytes into `arena` (current-device memory or page-locked host
+ * memory; 16-byte aligned; >= the capsule's bytes, CAP_E_SIZE otherwise;
+ * disjoint from the source arena) with one stream-ordered copy, and returns
+ * in *out a new header over `arena` with the same descriptor and the new
+ * tier.  Device -> host demotes, host -> device promotes; the source header
+ * and arena stay valid.  The caller owns both arenas; the library allocates
+ * nothing. */
+CAP_API int capsule_move(cap_capsule src, void* arena, uint64_t arena_bytes,
+                         void* stream, cap_capsule* out);
+
+/* Tier of a capsule's arena: CAP_TIER_DEVICE or CAP_TIER_HOST. */
+CAP_API int capsule_tier(cap_capsule cap, uint32_t* tier);
 
 /* Free the host header (the arena remains the caller's). */
 CAP_API int capsule_release(cap_capsule cap);

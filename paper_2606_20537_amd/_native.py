@@ -23,6 +23,8 @@ CAP_E_HIP = -7
 
 CAP_KIND_POSITIONAL = 0
 CAP_KIND_FIXED = 1
+CAP_TIER_DEVICE = 0
+CAP_TIER_HOST = 1
 CAP_DTYPE_F32 = 0
 CAP_DTYPE_BF16 = 1
 
@@ -67,6 +69,8 @@ SIGNATURES = [
     ("capsule_gather_restore", ct.c_int, [ct.POINTER(_vp), _u32, ct.POINTER(_i32), ct.POINTER(_vp), _u32, _vp]),
     ("capsule_info", ct.c_int, [_vp, ct.POINTER(_u64), ct.POINTER(_u64), ct.POINTER(_u64), ct.POINTER(_u64),
                                 ct.POINTER(_vp)]),
+    ("capsule_move", ct.c_int, [_vp, _vp, _u64, _vp, ct.POINTER(_vp)]),
+    ("capsule_tier", ct.c_int, [_vp, ct.POINTER(_u32)]),
     ("capsule_release", ct.c_int, [_vp]),
     ("capsule_digest_tokens", _u64, [ct.POINTER(_i32), _u64]),
     ("linattn_chunked_prefill", ct.c_int, [ct.POINTER(linattn_args), _vp]),
@@ -248,6 +252,23 @@ def capsule_info(cap):
                                                ct.byref(ar)))
     return {"P_aligned": int(P.value), "bytes": int(nb.value), "prefix_digest": int(pd.value),
             "deploy_key": int(dk.value), "arena": int(ar.value or 0)}
+
+
+def capsule_move(cap, arena, arena_bytes=None, stream=None):
+    """Copy a capsule into another arena (device memory, or a pinned host tensor)
+    and return a capsule over it: device -> host demotes, host -> device promotes."""
+    if arena_bytes is None:
+        arena_bytes = arena.numel() * arena.element_size()
+    h = _vp()
+    _check("capsule_move", load().capsule_move(cap.handle, _addr(arena), int(arena_bytes), _stream(stream),
+                                                ct.byref(h)))
+    return Capsule(h.value, arena)
+
+
+def capsule_tier(cap):
+    out = _u32(0)
+    _check("capsule_tier", load().capsule_tier(cap.handle, ct.byref(out)))
+    return int(out.value)
 
 
 def capsule_release(cap):

@@ -45,6 +45,7 @@ struct cap_capsule_s {
     uint64_t bytes = 0;
     const void* arena = nullptr;
     uint64_t arena_bytes = 0;
+    uint32_t tier = CAP_TIER_DEVICE;  // where the arena lives
     std::vector<uint64_t> row_bytes, rows;
     std::vector<uint32_t> kinds;
 };
@@ -111,6 +112,7 @@ bool same_layout(const cap_capsule_s* c, const cap_set_s* s) {
 int check_restore_target(const cap_capsule_s* c, const cap_set_s* s, uint64_t prefix_digest, bool check_prefix) {
     if (check_prefix && c->prefix_digest != prefix_digest) return CAP_E_DIGEST;
     if (c->deploy_key != s->deploy_key) return CAP_E_DIGEST;
+    if (c->tier != CAP_TIER_DEVICE) return CAP_E_STATE;  // promote it first (capsule_move)
     if (!same_layout(c, s)) return CAP_E_SIZE;
     if (c->P_aligned > s->max_position) return CAP_E_SIZE;
     const uint64_t a0 = (uint64_t)(uintptr_t)c->arena, a1 = a0 + c->bytes;
@@ -120,6 +122,23 @@ int check_restore_target(const cap_capsule_s* c, const cap_set_s* s, uint64_t pr
 }
 
 int launch_status(hipError_t e) { return e == hipSuccess ? CAP_OK : CAP_E_HIP; }
+
+// Tier of an arena: memory of the current device, or page-locked host memory
+// the device can address (hipHostMalloc).  Anything else -- pageable host
+// memory, another device's memory, managed memory -- is rejected.
+int arena_tier(const void* p, uint32_t* tier) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return CAP_E_HIP;
+    hipPointerAttribute_t a{};
+    if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+        (void)hipGetLastError();  // unknown pointers report an error; it is not sticky
+        return CAP_E_INVAL;
+    }
+    if (a.isManaged) return CAP_E_UNSUPPORTED;
+    if (a.type == hipMemoryTypeDevice && a.device == dev) { *tier = CAP_TIER_DEVICE; return CAP_OK; }
+    if (a.type == hipMemoryTypeHost && a.devicePointer != nullptr) { *tier = CAP_TIER_HOST; return CAP_OK; }
+    return CAP_E_INVAL;
+}
 
 }  // namespace
 
@@ -133,7 +152,7 @@ const char* cap_status_string(int status) {
         case CAP_E_DIGEST: return "digest or deployment key mismatch";
         case CAP_E_UNSUPPORTED: return "unsupported kind, shape or dtype";
         case CAP_E_ALIGN: return "pointer or size not 16-byte aligned";
-        case CAP_E_STATE: return "set position is not the aligned boundary";
+        case CAP_E_STATE: return "wrong state: set position is not the aligned boundary, or capsule not device-resident";
         case CAP_E_HIP: return "HIP runtime error";
         default: return "unknown status";
     }
@@ -247,9 +266,13 @@ int capsule_snapshot(cap_set live, uint64_t P, uint64_t prefix_digest, void* are
         if (overlaps(a0, a1, b.ptr, b.ptr + b.row_bytes * b.rows)) return CAP_E_INVAL;
     int rc = current_device_matches(live);
     if (rc != CAP_OK) return rc;
+    uint32_t tier = CAP_TIER_DEVICE;
+    rc = arena_tier(arena, &tier);
+    if (rc != CAP_OK) return rc;
 
     cap_capsule_s* c = new (std::nothrow) cap_capsule_s();
     if (!c) return CAP_E_INVAL;
+    c->tier = tier;
     c->P_requested = P;
     c->P_aligned = Pa;
     c->prefix_digest = prefix_digest;
@@ -402,6 +425,37 @@ int capsule_info(cap_capsule cap, uint64_t* P_aligned, uint64_t* bytes, uint64_t
     if (prefix_digest) *prefix_digest = cap->prefix_digest;
     if (deploy_key) *deploy_key = cap->deploy_key;
     if (arena) *arena = cap->arena;
+    return CAP_OK;
+}
+
+int capsule_move(cap_capsule src, void* arena, uint64_t arena_bytes, void* stream, cap_capsule* out) {
+    if (!out) return CAP_E_INVAL;
+    *out = nullptr;
+    if (!src || !arena) return CAP_E_INVAL;
+    if (!aligned16((uint64_t)(uintptr_t)arena)) return CAP_E_ALIGN;
+    if (arena_bytes < src->bytes) return CAP_E_SIZE;
+    const uint64_t s0 = (uint64_t)(uintptr_t)src->arena, d0 = (uint64_t)(uintptr_t)arena;
+    if (overlaps(s0, s0 + src->bytes, d0, d0 + src->bytes)) return CAP_E_INVAL;
+    uint32_t tier = CAP_TIER_DEVICE;
+    int rc = arena_tier(arena, &tier);
+    if (rc != CAP_OK) return rc;
+    cap_capsule_s* c = new (std::nothrow) cap_capsule_s(*src);
+    if (!c) return CAP_E_INVAL;
+    c->arena = arena;
+    c->arena_bytes = arena_bytes;
+    c->tier = tier;
+    if (src->bytes > 0 &&
+        hipMemcpyAsync(arena, src->arena, src->bytes, hipMemcpyDefault, static_cast<hipStream_t>(stream)) != hipSuccess) {
+        delete c;
+        return CAP_E_HIP;
+    }
+    *out = c;
+    return CAP_OK;
+}
+
+int capsule_tier(cap_capsule cap, uint32_t* tier) {
+    if (!cap || !tier) return CAP_E_INVAL;
+    *tier = cap->tier;
     return CAP_OK;
 }
 

@@ -118,6 +118,12 @@ def test_null_handles():
     assert L.capsule_fork(None, None, 0, 0, None) == cap.CAP_E_INVAL
     assert L.capsule_gather_restore(None, 0, None, None, 0, None) == cap.CAP_E_INVAL
     assert L.linattn_chunked_prefill(None, None) == cap.CAP_E_INVAL
+    h = ct.c_void_p(1)
+    assert L.capsule_move(None, None, 0, None, ct.byref(h)) == cap.CAP_E_INVAL
+    assert h.value is None
+    assert L.capsule_move(None, None, 0, None, None) == cap.CAP_E_INVAL
+    t = ct.c_uint32(9)
+    assert L.capsule_tier(None, ct.byref(t)) == cap.CAP_E_INVAL and t.value == 9
 
 
 def _args(**kw):

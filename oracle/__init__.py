@@ -52,6 +52,14 @@ class Oracle:
         L.orc_digest_tokens.restype = u64
         L.orc_digest_bytes.argtypes = [vp, u64]
         L.orc_digest_bytes.restype = u64
+        L.orc_e4m3_decode.argtypes = [ct.c_uint8]
+        L.orc_e4m3_decode.restype = ct.c_float
+        L.orc_e4m3_encode.argtypes = [ct.c_float]
+        L.orc_e4m3_encode.restype = ct.c_uint8
+        L.orc_bf16_round.argtypes = [ct.c_float]
+        L.orc_bf16_round.restype = ct.c_uint16
+        L.orc_fp8_quantize.argtypes = [vp, vp, u64, ct.c_float]
+        L.orc_fp8_dequantize.argtypes = [vp, vp, u64, ct.c_float]
         self.lib = L
 
     # ---- gated linear attention (§2 hybrid recurrent state; §5 chunking) ----
@@ -164,6 +172,32 @@ class Oracle:
     def digest_bytes(self, data: bytes):
         buf = (ct.c_ubyte * max(1, len(data))).from_buffer_copy(data or b"\0")
         return int(self.lib.orc_digest_bytes(ct.cast(buf, ct.c_void_p), len(data)))
+
+
+    # ---- FP8 KV region (§3 "Definition": FP8-KV halves the KV region; the
+    # BF16 working stage is rebuilt lazily, §3 cost model).  OCP E4M3.
+    def e4m3_decode(self, code: int) -> float:
+        return float(self.lib.orc_e4m3_decode(int(code) & 0xFF))
+
+    def e4m3_encode(self, x: float) -> int:
+        return int(self.lib.orc_e4m3_encode(float(np.float32(x))))
+
+    def bf16_round(self, y: float) -> int:
+        return int(self.lib.orc_bf16_round(float(np.float32(y))))
+
+    def fp8_quantize(self, src_bf16_bits, scale):
+        """uint16 bf16 bit patterns -> uint8 E4M3 codes of x / scale."""
+        src = np.ascontiguousarray(src_bf16_bits, dtype=np.uint16)
+        out = np.empty(src.shape, dtype=np.uint8)
+        self.lib.orc_fp8_quantize(_ptr(src), _ptr(out), src.size, float(np.float32(scale)))
+        return out
+
+    def fp8_dequantize(self, codes, scale):
+        """uint8 E4M3 codes -> uint16 bf16 bit patterns of decode(code) * scale."""
+        src = np.ascontiguousarray(codes, dtype=np.uint8)
+        out = np.empty(src.shape, dtype=np.uint16)
+        self.lib.orc_fp8_dequantize(_ptr(src), _ptr(out), src.size, float(np.float32(scale)))
+        return out
 
 
 _default = None

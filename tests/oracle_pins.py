@@ -393,4 +393,97 @@ def pin_digest(orc):
 CAPSULE_PINS = [pin_align, pin_capsule_size_table, pin_snapshot_layout,
                 pin_restore_roundtrip, pin_fork_and_gather, pin_digest]
 
-ALL_PINS = SCAN_PINS + CAPSULE_PINS
+
+# ------------------------------------------------------------- FP8 KV ----
+# OCP 8-bit floating point, E4M3 ("E4M3FN"): the format's published facts,
+# and torch's own float8_e4m3fn / bfloat16 conversions (an implementation
+# independent of the oracle) over the range where both define the result.
+def pin_e4m3_published_values(orc):
+    """Largest finite 448 = S.1111.110, smallest normal 2^-6 = 0.0001.000,
+    smallest subnormal 2^-9, largest subnormal 7/8 * 2^-6, one = 0.0111.000,
+    NaN = S.1111.111, no infinities; the negative half mirrors the positive."""
+    assert orc.e4m3_decode(0x7E) == 448.0
+    assert orc.e4m3_decode(0x08) == 2.0 ** -6
+    assert orc.e4m3_decode(0x01) == 2.0 ** -9
+    assert orc.e4m3_decode(0x07) == 0.875 * 2.0 ** -6
+    assert orc.e4m3_decode(0x38) == 1.0
+    assert np.isnan(orc.e4m3_decode(0x7F)) and np.isnan(orc.e4m3_decode(0xFF))
+    vals = [orc.e4m3_decode(c) for c in range(0x7F)]
+    assert all(np.isfinite(vals)) and all(b > a for a, b in zip(vals, vals[1:]))   # strictly increasing
+    for c in range(0x7F):
+        assert orc.e4m3_decode(c | 0x80) == -orc.e4m3_decode(c) or c == 0
+
+
+def pin_e4m3_against_torch(orc):
+    """Every code decodes as torch's float8_e4m3fn does; encoding agrees with
+    torch's round-to-nearest-even cast on |x| < 464 (beyond that torch gives
+    NaN, the oracle saturates to 448 -- the reading taken)."""
+    import torch
+    codes = np.arange(256, dtype=np.uint8)
+    tv = torch.from_numpy(codes).view(torch.float8_e4m3fn).float().numpy()
+    for c in range(256):
+        ov = orc.e4m3_decode(c)
+        assert (np.isnan(ov) and np.isnan(tv[c])) or ov == tv[c], c
+    r = rng(11, 0, "fp8pin")
+    xs = np.concatenate([r.standard_normal(3000) * 10.0, r.uniform(-463.9, 463.9, 2000),
+                         r.standard_normal(2000) * 2.0 ** -8,
+                         (np.array([tv[c] for c in range(0x7E)]) + np.array([tv[c + 1] for c in range(0x7E)])) / 2,
+                         -(np.array([tv[c] for c in range(0x7E)]) + np.array([tv[c + 1] for c in range(0x7E)])) / 2])
+    xs = xs.astype(np.float32)
+    want = torch.from_numpy(xs).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    for x, w in zip(xs, want):
+        assert orc.e4m3_encode(x) == w, (float(x), orc.e4m3_encode(x), int(w))
+
+
+def pin_e4m3_round_trip_and_saturation(orc):
+    """encode(decode(c)) = c for every finite code; values at or beyond 448
+    (and +-inf) saturate to +-448; NaN keeps its sign; the error of a
+    normal-range value is at most half a unit in the last place: 2^-4 relative."""
+    for c in range(256):
+        if (c & 0x7F) == 0x7F:
+            continue
+        assert orc.e4m3_encode(orc.e4m3_decode(c)) == c, c
+    for x, want in [(448.0, 0x7E), (449.0, 0x7E), (1e30, 0x7E), (float("inf"), 0x7E),
+                    (-1e30, 0xFE), (float("-inf"), 0xFE), (float("nan"), 0x7F), (-float("nan"), 0xFF)]:
+        assert orc.e4m3_encode(x) == want, (x, want)
+    r = rng(12, 0, "fp8pin")
+    xs = (r.uniform(2.0 ** -6, 440.0, 4000) * r.choice([-1.0, 1.0], 4000)).astype(np.float32)
+    for x in xs:
+        y = orc.e4m3_decode(orc.e4m3_encode(x))
+        assert abs(y - float(x)) <= abs(float(x)) * 2.0 ** -4, (float(x), y)
+
+
+def pin_fp8_arrays_scale_and_bf16(orc):
+    """The array forms apply the scale (stored value x / scale, restored
+    value code * scale), rounding to bf16 as torch's float -> bfloat16 cast
+    does (round to nearest even)."""
+    import torch
+    r = rng(13, 0, "fp8pin")
+    x = r.standard_normal(4096).astype(np.float32) * 3.0
+    bits = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    xb = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).float().numpy()
+    for scale in (1.0, 0.03125, 2.5):
+        q = orc.fp8_quantize(bits, scale)
+        inv = np.float32(1.0) / np.float32(scale)
+        tq = torch.from_numpy((xb * inv).astype(np.float32)).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+        sat = np.abs(xb * inv) >= 448.0
+        assert np.array_equal(q[~sat], tq[~sat]), scale
+        assert np.all(q[sat & (xb > 0)] == 0x7E) and np.all(q[sat & (xb < 0)] == 0xFE)
+        d = orc.fp8_dequantize(q, scale)
+        fv = torch.from_numpy(q).view(torch.float8_e4m3fn).float().numpy() * np.float32(scale)
+        td = torch.from_numpy(fv.astype(np.float32)).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+        assert np.array_equal(d, td), scale
+    ys = r.standard_normal(20000).astype(np.float32) * np.float32(2.0) ** r.integers(-20, 20, 20000).astype(np.float32)
+    # exact midpoints between neighbouring bf16 values: ties go to the even one
+    base = (r.integers(0x0080, 0x7F00, 2000).astype(np.uint32) << 16) | (r.integers(0, 2, 2000).astype(np.uint32) << 31)
+    mids = (base | 0x8000).view(np.float32)
+    ys = np.concatenate([ys[:3000], mids])
+    tb = torch.from_numpy(ys).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    for y, w in zip(ys, tb):
+        assert orc.bf16_round(y) == w, (float(y), orc.bf16_round(y), int(w))
+
+
+FP8_PINS = [pin_e4m3_published_values, pin_e4m3_against_torch, pin_e4m3_round_trip_and_saturation,
+            pin_fp8_arrays_scale_and_bf16]
+
+ALL_PINS = SCAN_PINS + CAPSULE_PINS + FP8_PINS

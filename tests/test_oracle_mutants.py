@@ -13,7 +13,7 @@ import pytest
 
 import oracle
 from oracle import build as obuild
-from oracle_pins import CAPSULE_PINS, SCAN_PINS
+from oracle_pins import CAPSULE_PINS, FP8_PINS, SCAN_PINS
 
 ORACLE_DIR = os.path.dirname(os.path.abspath(oracle.__file__))
 
@@ -54,6 +54,20 @@ MUTANTS = [
      "h *= 1099511628211ULL;", "h *= 1099511628213ULL;", "capsule"),
     ("gather_ignores_ids", "capsule_oracle.c",
      "gallery[ids[e]]);", "gallery[e % n_gallery]);", "capsule"),
+    ("e4m3_bias_off_by_one", "fp8_oracle.c",
+     "return ldexp(1.0 + (double)m / 8.0, (int)e - 7);", "return ldexp(1.0 + (double)m / 8.0, (int)e - 8);", "fp8"),
+    ("e4m3_subnormal_scale", "fp8_oracle.c",
+     "return ldexp((double)m / 8.0, -6);", "return ldexp((double)m / 8.0, -7);", "fp8"),
+    ("e4m3_ties_to_odd", "fp8_oracle.c",
+     "(d == best_d && (c & 1u) == 0u)", "(d == best_d && (c & 1u) == 1u)", "fp8"),
+    ("e4m3_overflow_to_nan", "fp8_oracle.c",
+     "if (a >= 448.0) return (uint8_t)(sign | 0x7Eu);", "if (a >= 448.0) return (uint8_t)(sign | 0x7Fu);", "fp8"),
+    ("fp8_quantize_multiplies_by_scale", "fp8_oracle.c",
+     "const float x = bf16_value(src_bf16[i]) * inv;", "const float x = bf16_value(src_bf16[i]) * scale;", "fp8"),
+    ("fp8_dequantize_drops_scale", "fp8_oracle.c",
+     "const float y = orc_e4m3_decode(c) * scale;", "const float y = orc_e4m3_decode(c);", "fp8"),
+    ("bf16_ties_away", "fp8_oracle.c",
+     "return (uint16_t)(((lo >> 16) & 1u) ? (hi >> 16) : (lo >> 16));", "return (uint16_t)(hi >> 16);", "fp8"),
 ]
 
 
@@ -68,7 +82,7 @@ def test_mutant_is_caught(tmp_path, mid, fname, old, new, family):
     (src / fname).write_text(text.replace(old, new))
     lib = obuild.build(out_path=str(tmp_path / ("liborc_%s.so" % mid)), src_dir=str(src))
     mutant = oracle.Oracle(lib)
-    pins = SCAN_PINS if family == "scan" else CAPSULE_PINS
+    pins = {"scan": SCAN_PINS, "capsule": CAPSULE_PINS, "fp8": FP8_PINS}[family]
     caught = []
     for pin in pins:
         try:

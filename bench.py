@@ -280,6 +280,13 @@ def main():
     ms = {k: float(np.mean([r[0][k][0].elapsed_time(r[0][k][1]) for r in recs])) for k in phases}
     ms_per_step = wall * 1e3 / args.steps
 
+    # post-run spot check: every fork branch holds the capsule's bytes (the
+    # set starts with lin0.state; KV is not touched by the continuation)
+    nst = H * dk * dv * 4
+    for fl, fk in fork_keep:
+        assert torch.equal(fl[0]["state"].view(torch.uint8).flatten(), arena[:nst])
+        assert torch.equal(fk[-1][1][: P * w.kv_row_bytes], kv[-1][1][: P * w.kv_row_bytes])
+
     # ---- host tier, outside the timed step: demote the capsule to pinned
     # host memory and promote it back (each a stream-ordered copy over the
     # host link), one warm-up and three timed rounds, checked bitwise
@@ -302,13 +309,53 @@ def main():
     assert cap.capsule_tier(c_host) == cap.CAP_TIER_HOST and cap.capsule_tier(c_back) == cap.CAP_TIER_DEVICE
     assert torch.equal(d_arena, arena)
     demote_ms, promote_ms = float(np.median(tier_ms["demote"])), float(np.median(tier_ms["promote"]))
+    del h_arena, d_arena
 
-    # post-run spot check: every fork branch holds the capsule's bytes (the
-    # set starts with lin0.state; KV is not touched by the continuation)
-    nst = H * dk * dv * 4
-    for fl, fk in fork_keep:
-        assert torch.equal(fl[0]["state"].view(torch.uint8).flatten(), arena[:nst])
-        assert torch.equal(fk[-1][1][: P * w.kv_row_bytes], kv[-1][1][: P * w.kv_row_bytes])
+    # ---- FP8 KV region, outside the timed step: the 24 K/V buffers held as
+    # OCP E4M3 (one byte per element, scale 1), quantized from the bf16 rows
+    # [0, P) in one launch; a live set over the FP8 regions and the same
+    # states and conv tails; its snapshot / restore; and the lazy rebuild of
+    # the bf16 stage (here: the bf16 K/V buffers themselves) over [0, P')
+    kv_el = w.kv_row_bytes // 2
+    fp8 = [(name, torch.empty(w.t_max * kv_el, dtype=torch.uint8, device=dev)) for name, _ in kv]
+    quant_segs = [(t, f, P * kv_el, 1.0) for (_, t), (_, f) in zip(kv, fp8)]
+    stage_segs = [(f, t, P * kv_el, 1.0) for (_, t), (_, f) in zip(kv, fp8)]
+
+    def fp8_bufs():
+        out = []
+        for b in live_bufs(layers, fp8):
+            name, t, rb, rows, kind = b
+            out.append((name, t, kv_el if kind == cap.CAP_KIND_POSITIONAL else rb, rows, kind))
+        return out
+
+    live8 = cap.cap_set_create(fp8_bufs(), w.chunk, deploy)
+    cap.cap_set_set_position(live8, P)
+    cap8_bytes = cap.capsule_bytes(live8, P)
+    arena8 = torch.empty(cap8_bytes, dtype=torch.uint8, device=dev)
+    f8 = {"quantize": [], "snapshot": [], "restore": [], "rebuild": []}
+    with torch.cuda.stream(stream):
+        for rnd in range(4):
+            t = {}
+            for name, fn in [("quantize", lambda: cap.kv_fp8_quantize(quant_segs, stream=stream)),
+                             ("snapshot", lambda: t.__setitem__("c8", cap.capsule_snapshot(live8, P, digest, arena8,
+                                                                                          stream=stream))),
+                             ("restore", lambda: cap.capsule_restore(t["c8"], live8, digest, stream=stream)),
+                             ("rebuild", lambda: cap.kv_fp8_dequantize(stage_segs, stream=stream))]:
+                flush.fill_(rnd)
+                e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+                e[0].record(stream)
+                fn()
+                e[1].record(stream)
+                stream.synchronize()
+                if rnd:
+                    f8[name].append(e[0].elapsed_time(e[1]))
+    f8ms = {k: float(np.median(v)) for k, v in f8.items()}
+    conv_bytes = P * kv_el * len(kv) * 3  # read 2 + write 1 (quantize) or read 1 + write 2 (rebuild)
+    # the rebuilt stage reproduces the quantized rows exactly (scale 1 keeps N(0,1) bf16 values in range)
+    chk = torch.empty(P * kv_el, dtype=torch.bfloat16, device=dev)
+    cap.kv_fp8_dequantize([(fp8[0][1], chk, P * kv_el, 1.0)], stream=stream)
+    stream.synchronize()
+    assert torch.equal(chk, kv[0][1][: 2 * P * kv_el].view(torch.bfloat16))
 
     scan_b = scan_bytes(T, H, dk, dv, True)
     scan_b_final = scan_bytes(T, H, dk, dv, False)
@@ -361,6 +408,16 @@ def main():
                       "link": "host link, PCIe 5.0 x16", "peak": LINK_PEAK_GBS, "unit": "GB/s",
                       "promote_frac": round(cap_bytes / (promote_ms * 1e-3) / 1e9 / LINK_PEAK_GBS, 4),
                       "capsule_ttft_ms_from_host": round(promote_ms + ms["restore"] + ms["continue"], 4)},
+        "fp8_kv": {"capsule_bytes": cap8_bytes, "bf16_capsule_bytes": cap_bytes,
+                   "restore_ms": round(f8ms["restore"], 4), "snapshot_ms": round(f8ms["snapshot"], 4),
+                   "restore_gbs": round(2 * cap8_bytes / (f8ms["restore"] * 1e-3) / 1e9, 2),
+                   "rebuild_ms": round(f8ms["rebuild"], 4),
+                   "rebuild_gbs": round(conv_bytes / (f8ms["rebuild"] * 1e-3) / 1e9, 2),
+                   "rebuild_frac": round(conv_bytes / (f8ms["rebuild"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                   "quantize_ms": round(f8ms["quantize"], 4),
+                   "quantize_gbs": round(conv_bytes / (f8ms["quantize"] * 1e-3) / 1e9, 2),
+                   "capsule_ttft_ms": round(f8ms["restore"] + f8ms["rebuild"] + ms["continue"], 4),
+                   "capsule_ttft_ms_lazy_none": round(f8ms["restore"] + ms["continue"], 4)},
         "setup_s": round(t_setup, 1),
     }
     if not args.no_cpu_baseline:

@@ -257,6 +257,46 @@ typedef struct linattn_args {
 
 CAP_API int linattn_chunked_prefill(const linattn_args* args, void* stream);
 
+/* ---------------------------------------------------------- FP8 KV ------ */
+/* §3 "Definition": the KV region may be held in FP8, which roughly halves
+ * the capsule (an FP8 K or V buffer is an ordinary POSITIONAL buffer with
+ * one byte per element); the BF16 working stage read by the attention is not
+ * part of the capsule and is rebuilt lazily after a restore (§3 cost model:
+ * restore copies bytes and rebinds; the stage of a restored session is valid
+ * over no rows until rebuilt with kv_fp8_dequantize).
+ *
+ * Format: OCP 8-bit floating point E4M3 (sign, 4 exponent bits with bias 7,
+ * 3 mantissa bits; largest finite 448; S.1111.111 is NaN; no infinities),
+ * one fp32 scale per segment, stored value = x / scale.
+ *
+ * A segment converts n elements (n % 16 == 0) from src to dst, both device
+ * pointers, 16-byte aligned (CAP_E_ALIGN), caller-owned, disjoint (src from
+ * dst, and the destinations of one call from each other: CAP_E_INVAL).
+ * scale must be finite and > 0 (CAP_E_INVAL); reserved must be 0.  Up to
+ * KV_FP8_MAX_SEG segments (one per K or V buffer) run in one launch;
+ * segments with n = 0 are skipped. */
+#define KV_FP8_MAX_SEG 64
+
+typedef struct kv_fp8_seg {
+    const void* src;
+    void*       dst;
+    uint64_t    n;         /* elements */
+    float       scale;
+    uint32_t    reserved;
+} kv_fp8_seg;
+
+/* bf16 -> E4M3: code = nearest representable value to float(x) * (1.0f /
+ * scale) (fp32 product), ties to the even mantissa; |value| >= 448 and +-inf
+ * saturate to +-448, NaN keeps its sign.  Appended K/V rows enter the FP8
+ * region this way. */
+CAP_API int kv_fp8_quantize(const kv_fp8_seg* segs, uint32_t n_seg, void* stream);
+
+/* E4M3 -> bf16: decode(code) * scale in fp32, rounded to the nearest bf16
+ * (ties to even); NaN codes give the canonical bf16 NaN with the code's
+ * sign.  Rebuilds the BF16 stage of a row range (the lazy rebuild after a
+ * restore). */
+CAP_API int kv_fp8_dequantize(const kv_fp8_seg* segs, uint32_t n_seg, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

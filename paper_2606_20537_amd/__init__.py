@@ -11,5 +11,6 @@ from ._native import (  # noqa: F401
     CAP_MAX_GALLERY, CAP_OK, CAP_TIER_DEVICE, CAP_TIER_HOST, SIGNATURES, CapSet, Capsule, CapsuleError, cap_align_boundary, cap_set_create,
     cap_set_destroy, cap_set_get_position, cap_set_set_position, cap_status_string, capsule_bytes,
     capsule_digest_tokens, capsule_fork, capsule_gather_restore, capsule_info, capsule_layout_bytes,
-    capsule_move, capsule_release, capsule_restore, capsule_snapshot, capsule_tier, linattn_chunked_prefill, load,
+    capsule_move, capsule_release, capsule_restore, capsule_snapshot, capsule_tier, kv_fp8_dequantize, kv_fp8_quantize,
+    linattn_chunked_prefill, load,
 )

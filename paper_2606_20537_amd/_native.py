@@ -52,6 +52,11 @@ class linattn_args(ct.Structure):
                 ("dv", ct.c_int32), ("chunk", ct.c_int32), ("in_dtype", ct.c_int32), ("scale", ct.c_float)]
 
 
+class kv_fp8_seg(ct.Structure):
+    _fields_ = [("src", ct.c_void_p), ("dst", ct.c_void_p), ("n", ct.c_uint64), ("scale", ct.c_float),
+                ("reserved", ct.c_uint32)]
+
+
 # (name, restype, argtypes) of every exported entry point
 _vp, _u64, _u32, _i32 = ct.c_void_p, ct.c_uint64, ct.c_uint32, ct.c_int32
 SIGNATURES = [
@@ -70,6 +75,8 @@ SIGNATURES = [
     ("capsule_info", ct.c_int, [_vp, ct.POINTER(_u64), ct.POINTER(_u64), ct.POINTER(_u64), ct.POINTER(_u64),
                                 ct.POINTER(_vp)]),
     ("capsule_move", ct.c_int, [_vp, _vp, _u64, _vp, ct.POINTER(_vp)]),
+    ("kv_fp8_quantize", ct.c_int, [ct.POINTER(kv_fp8_seg), _u32, _vp]),
+    ("kv_fp8_dequantize", ct.c_int, [ct.POINTER(kv_fp8_seg), _u32, _vp]),
     ("capsule_tier", ct.c_int, [_vp, ct.POINTER(_u32)]),
     ("capsule_release", ct.c_int, [_vp]),
     ("capsule_digest_tokens", _u64, [ct.POINTER(_i32), _u64]),
@@ -294,3 +301,24 @@ def linattn_chunked_prefill(q, k, v, g, o, *, state_in=None, chunk_states=None, 
     a = linattn_args(_addr(q), _addr(k), _addr(v), _addr(g), _addr(state_in), _addr(o), _addr(chunk_states),
                      _addr(final_state), int(T), int(H), int(dk), int(dv), int(chunk), int(in_dtype), float(scale))
     return _check("linattn_chunked_prefill", load().linattn_chunked_prefill(ct.byref(a), _stream(stream)))
+
+
+def _fp8_segs(segs):
+    """segs: iterable of (src, dst, n_elements, scale); src/dst tensors or addresses."""
+    segs = list(segs)
+    arr = (kv_fp8_seg * max(1, len(segs)))()
+    for i, (src, dst, n, scale) in enumerate(segs):
+        arr[i] = kv_fp8_seg(_addr(src), _addr(dst), int(n), float(scale), 0)
+    return arr, len(segs)
+
+
+def kv_fp8_quantize(segs, stream=None):
+    """bf16 -> OCP E4M3 for each (src, dst, n, scale) segment, one launch."""
+    arr, n = _fp8_segs(segs)
+    return _check("kv_fp8_quantize", load().kv_fp8_quantize(arr, n, _stream(stream)))
+
+
+def kv_fp8_dequantize(segs, stream=None):
+    """OCP E4M3 -> bf16 for each (src, dst, n, scale) segment, one launch."""
+    arr, n = _fp8_segs(segs)
+    return _check("kv_fp8_dequantize", load().kv_fp8_dequantize(arr, n, _stream(stream)))

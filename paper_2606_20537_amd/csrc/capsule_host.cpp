@@ -6,6 +6,7 @@
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdlib>
 #include <cstring>
 #include <new>
@@ -463,6 +464,54 @@ int capsule_release(cap_capsule cap) {
     if (!cap) return CAP_E_INVAL;
     delete cap;
     return CAP_OK;
+}
+
+// ------------------------------------------------------------ FP8 KV ----
+static int fp8_convert(const kv_fp8_seg* segs, uint32_t n_seg, void* stream, bool quantize) {
+    if (!segs || n_seg == 0) return CAP_E_INVAL;
+    if (n_seg > KV_FP8_MAX_SEG) return CAP_E_UNSUPPORTED;
+    const uint64_t src_es = quantize ? 2 : 1, dst_es = quantize ? 1 : 2;
+    std::vector<std::pair<uint64_t, uint64_t>> dst_ranges;
+    for (uint32_t i = 0; i < n_seg; ++i) {
+        const kv_fp8_seg& g = segs[i];
+        if (g.reserved != 0) return CAP_E_INVAL;
+        if (!(g.scale > 0.0f) || !std::isfinite(g.scale)) return CAP_E_INVAL;
+        if (g.n == 0) continue;
+        if (!g.src || !g.dst) return CAP_E_INVAL;
+        if ((g.n & 15u) != 0 || !aligned16((uint64_t)(uintptr_t)g.src) || !aligned16((uint64_t)(uintptr_t)g.dst))
+            return CAP_E_ALIGN;
+        if (g.n > (UINT64_MAX / 4)) return CAP_E_SIZE;
+        const uint64_t s0 = (uint64_t)(uintptr_t)g.src, d0 = (uint64_t)(uintptr_t)g.dst;
+        if (overlaps(s0, s0 + g.n * src_es, d0, d0 + g.n * dst_es)) return CAP_E_INVAL;
+        dst_ranges.emplace_back(d0, d0 + g.n * dst_es);
+    }
+    std::sort(dst_ranges.begin(), dst_ranges.end());
+    for (size_t i = 1; i < dst_ranges.size(); ++i)
+        if (dst_ranges[i].first < dst_ranges[i - 1].second) return CAP_E_INVAL;
+    cap::Fp8Params p{};
+    uint64_t blocks = 0;
+    for (uint32_t i = 0; i < n_seg; ++i) {
+        const kv_fp8_seg& g = segs[i];
+        p.src[i] = (uint64_t)(uintptr_t)g.src;
+        p.dst[i] = (uint64_t)(uintptr_t)g.dst;
+        p.n_groups[i] = g.n / 16;
+        p.mul[i] = quantize ? 1.0f / g.scale : g.scale;
+        p.first_block[i] = (uint32_t)blocks;
+        blocks += (p.n_groups[i] + cap::kFp8GroupsPerBlock - 1) / cap::kFp8GroupsPerBlock;
+        if (blocks > 0x7fffffffull) return CAP_E_SIZE;
+    }
+    p.first_block[n_seg] = (uint32_t)blocks;
+    p.n_seg = n_seg;
+    p.quantize = quantize ? 1 : 0;
+    return launch_status(cap::launch_fp8(p, static_cast<hipStream_t>(stream)));
+}
+
+int kv_fp8_quantize(const kv_fp8_seg* segs, uint32_t n_seg, void* stream) {
+    return fp8_convert(segs, n_seg, stream, true);
+}
+
+int kv_fp8_dequantize(const kv_fp8_seg* segs, uint32_t n_seg, void* stream) {
+    return fp8_convert(segs, n_seg, stream, false);
 }
 
 uint64_t capsule_digest_tokens(const int32_t* ids, uint64_t n) {

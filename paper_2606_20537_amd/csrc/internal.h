@@ -1,5 +1,6 @@
 // Internal interface between the host ABI (capsule_host.cpp) and the HIP
-// kernels (capsule_copy.hip, linattn_scan.hip).  Not part of the public ABI.
+// kernels (capsule_copy.hip, linattn_scan.hip, kv_fp8.hip).  Not part of the
+// public ABI.
 #pragma once
 
 #include <hip/hip_runtime_api.h>
@@ -65,5 +66,25 @@ struct ScanParams {
 };
 
 hipError_t launch_linattn_scan(const ScanParams& p, hipStream_t stream);
+
+// FP8 (OCP E4M3) conversion of up to kFp8MaxSeg segments in one launch.
+// Segment s converts n_groups[s] groups of 16 elements from src[s] to
+// dst[s]; block b of the grid works on segment s with first_block[s] <= b <
+// first_block[s + 1].  Quantize multiplies by mul[s] (1 / scale) before
+// encoding; dequantize multiplies the decoded value by mul[s] (scale).
+constexpr int kFp8MaxSeg = 64;
+constexpr int kFp8GroupsPerBlock = 512;  // 256 threads x 2 groups of 16 elements
+
+struct Fp8Params {
+    uint64_t src[kFp8MaxSeg];
+    uint64_t dst[kFp8MaxSeg];
+    uint64_t n_groups[kFp8MaxSeg];
+    uint32_t first_block[kFp8MaxSeg + 1];
+    float    mul[kFp8MaxSeg];
+    uint32_t n_seg;
+    int32_t  quantize;  // 1: bf16 -> e4m3, 0: e4m3 -> bf16
+};
+
+hipError_t launch_fp8(const Fp8Params& p, hipStream_t stream);
 
 }  // namespace cap

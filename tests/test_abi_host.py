@@ -161,3 +161,31 @@ def test_scan_argument_checks():
 def test_python_binding_has_no_fallback(tmp_path):
     with pytest.raises(ImportError):
         N.load(str(tmp_path / "missing.so"))
+
+
+def _fp8_status(segs, quantize=True):
+    arr = (N.kv_fp8_seg * max(1, len(segs)))()
+    for i, (src, dst, n, scale, res) in enumerate(segs):
+        arr[i] = N.kv_fp8_seg(src, dst, n, scale, res)
+    fn = N.load().kv_fp8_quantize if quantize else N.load().kv_fp8_dequantize
+    return fn(arr, len(segs), None)
+
+
+def test_fp8_argument_checks():
+    ok = (1 << 20, 1 << 24, 1024, 1.0, 0)
+    for q in (True, False):
+        assert N.load().kv_fp8_quantize(None, 1, None) == cap.CAP_E_INVAL
+        assert _fp8_status([], q) == cap.CAP_E_INVAL
+        assert _fp8_status([ok] * 65, q) == cap.CAP_E_UNSUPPORTED
+        assert _fp8_status([(1 << 20, 1 << 24, 1000, 1.0, 0)], q) == cap.CAP_E_ALIGN     # n % 16
+        assert _fp8_status([((1 << 20) + 8, 1 << 24, 1024, 1.0, 0)], q) == cap.CAP_E_ALIGN
+        assert _fp8_status([(1 << 20, 1 << 24, 1024, 0.0, 0)], q) == cap.CAP_E_INVAL
+        assert _fp8_status([(1 << 20, 1 << 24, 1024, -1.0, 0)], q) == cap.CAP_E_INVAL
+        assert _fp8_status([(1 << 20, 1 << 24, 1024, float("nan"), 0)], q) == cap.CAP_E_INVAL
+        assert _fp8_status([(1 << 20, 1 << 24, 1024, float("inf"), 0)], q) == cap.CAP_E_INVAL
+        assert _fp8_status([(1 << 20, 1 << 24, 1024, 1.0, 1)], q) == cap.CAP_E_INVAL
+        assert _fp8_status([(0, 1 << 24, 1024, 1.0, 0)], q) == cap.CAP_E_INVAL
+        assert _fp8_status([(1 << 20, (1 << 20) + 512, 1024, 1.0, 0)], q) == cap.CAP_E_INVAL   # src/dst overlap
+        two = [(1 << 20, 1 << 24, 1024, 1.0, 0), (1 << 21, (1 << 24) + 512, 1024, 1.0, 0)]
+        assert _fp8_status(two, q) == cap.CAP_E_INVAL                                        # dst overlap
+

@@ -48,6 +48,8 @@ class Oracle:
         L.orc_capsule_fork.argtypes = [u32, u32, vp, vp, vp, vp, u64, vp]
         L.orc_capsule_gather.argtypes = [u32, u32, vp, vp, vp, vp, u64, u32, vp, vp]
         L.orc_capsule_gather.restype = ct.c_int
+        L.orc_set_append.argtypes = [u32, vp, vp, vp, vp, vp, u64, u64, vp]
+        L.orc_set_append.restype = ct.c_int
         L.orc_digest_tokens.argtypes = [vp, u64]
         L.orc_digest_tokens.restype = u64
         L.orc_digest_bytes.argtypes = [vp, u64]
@@ -145,6 +147,19 @@ class Oracle:
         arena = np.ascontiguousarray(arena, dtype=np.uint8)
         self.lib.orc_capsule_restore(len(rb), self._ptr_array(bufs), _ptr(rb), _ptr(rt), _ptr(kd),
                                      int(P_aligned), _ptr(arena))
+
+    def append(self, bufs, srcs, row_bytes, rows_total, kinds, position, n):
+        """Append n rows at ``position`` into host buffers ``bufs`` (in place):
+        positional buffers get rows [position, position + n) from their source,
+        fixed buffers slide as windows; ``srcs[i]`` None leaves buffer i alone.
+        Returns the oracle's status (0, or -1 if a positional buffer is full)."""
+        rb, rt, kd = self._layout(row_bytes, rows_total, kinds)
+        keep = [None if x is None else np.ascontiguousarray(x) for x in srcs]
+        src_arr = (ct.c_void_p * len(srcs))(*[None if x is None else x.ctypes.data for x in keep])
+        width = max([int(rb[i] * (rt[i] + n)) for i in range(len(rb))] + [1])
+        scratch = np.empty(width, np.uint8)
+        return int(self.lib.orc_set_append(len(rb), self._ptr_array(bufs), src_arr, _ptr(rb), _ptr(rt), _ptr(kd),
+                                           int(position), int(n), _ptr(scratch)))
 
     def fork(self, arena, sets, row_bytes, rows_total, kinds, P_aligned):
         """Restore the same capsule into each buffer list of ``sets``."""

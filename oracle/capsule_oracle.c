@@ -105,6 +105,39 @@ int orc_capsule_gather(uint32_t n, uint32_t n_env, void* const* sets, const uint
     return 0;
 }
 
+/* append of n tokens at `position` (§3 Algorithm 1 restore: after the copy
+   the suffix is appended; §3 "Definition": the KV region is positional, the
+   convolution state is a fixed-size window of the latest inputs).  For every
+   buffer i with a source (srcs[i] != NULL, n rows of row_bytes[i] bytes):
+     positional: rows [position, position + n) <- the n source rows
+                 (-1 and nothing copied if position + n > rows_total[i]);
+     fixed:      the buffer is a window of its rows_total rows holding the
+                 latest rows of a history; it becomes the last rows_total rows
+                 of (its current rows followed by the n source rows).
+   Buffers without a source are untouched.  Returns 0 on success. */
+int orc_set_append(uint32_t n_buf, void* const* bufs, const void* const* srcs, const uint64_t* row_bytes,
+                   const uint64_t* rows_total, const uint32_t* kinds, uint64_t position, uint64_t n,
+                   unsigned char* scratch)
+{
+    for (uint32_t i = 0; i < n_buf; ++i)
+        if (srcs[i] && kinds[i] == ORC_KIND_POSITIONAL && position + n > rows_total[i]) return -1;
+    for (uint32_t i = 0; i < n_buf; ++i) {
+        if (!srcs[i] || n == 0) continue;
+        const uint64_t rb = row_bytes[i];
+        unsigned char* dst = (unsigned char*)bufs[i];
+        if (kinds[i] == ORC_KIND_POSITIONAL) {
+            memcpy(dst + position * rb, srcs[i], (size_t)(n * rb));
+        } else {
+            /* history = current window rows, then the new rows; keep its tail */
+            const uint64_t W = rows_total[i];
+            memcpy(scratch, dst, (size_t)(W * rb));
+            memcpy(scratch + W * rb, srcs[i], (size_t)(n * rb));
+            memcpy(dst, scratch + n * rb, (size_t)(W * rb));
+        }
+    }
+    return 0;
+}
+
 /* 64-bit FNV-1a (offset basis 14695981039346656037, prime 1099511628211)
    over the little-endian bytes of n int32 token ids. */
 uint64_t orc_digest_tokens(const int32_t* ids, uint64_t n)

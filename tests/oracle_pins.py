@@ -390,8 +390,42 @@ def pin_digest(orc):
     assert orc.digest_tokens(ids[:0]) == int("cbf29ce484222325", 16)
 
 
+def pin_append_history(orc):
+    """Append of a suffix, brute force: a positional buffer equals the token
+    history written row by row at its positions; a fixed window equals the
+    last W rows of its full history (initial rows, then every appended row),
+    for suffixes shorter than, equal to and longer than the window; buffers
+    without a source keep their bytes; a positional overflow copies nothing."""
+    r = rng(21, 0, "appendpin")
+    rb_pos, rows_pos, rb_win, W = 48, 40, 32, 4
+    kinds = [0, 1, 1]
+    rbs, rts = [rb_pos, rb_win, 64], [rows_pos, W, 2]
+    pos_buf = r.integers(0, 256, rows_pos * rb_pos, dtype=np.uint8)
+    win_buf = r.integers(0, 256, W * rb_win, dtype=np.uint8)
+    fixed = r.integers(0, 256, 128, dtype=np.uint8)
+    fixed0 = fixed.copy()
+    pos_hist = pos_buf.reshape(rows_pos, rb_pos).copy()
+    win_hist = list(win_buf.reshape(W, rb_win).copy())
+    position = 5
+    for n in (1, 2, 4, 7, 1, 3):
+        src_pos = r.integers(0, 256, n * rb_pos, dtype=np.uint8)
+        src_win = r.integers(0, 256, n * rb_win, dtype=np.uint8)
+        assert orc.append([pos_buf, win_buf, fixed], [src_pos, src_win, None], rbs, rts, kinds, position, n) == 0
+        pos_hist[position:position + n] = src_pos.reshape(n, rb_pos)
+        win_hist.extend(src_win.reshape(n, rb_win))
+        position += n
+        assert np.array_equal(pos_buf.reshape(rows_pos, rb_pos), pos_hist)
+        assert np.array_equal(win_buf.reshape(W, rb_win), np.stack(win_hist[-W:]))
+        assert np.array_equal(fixed, fixed0)
+    before = pos_buf.copy(), win_buf.copy()
+    src_pos = r.integers(0, 256, 20 * rb_pos, dtype=np.uint8)
+    src_win = r.integers(0, 256, 20 * rb_win, dtype=np.uint8)
+    assert orc.append([pos_buf, win_buf, fixed], [src_pos, src_win, None], rbs, rts, kinds, 30, 20) == -1
+    assert np.array_equal(pos_buf, before[0]) and np.array_equal(win_buf, before[1])
+
+
 CAPSULE_PINS = [pin_align, pin_capsule_size_table, pin_snapshot_layout,
-                pin_restore_roundtrip, pin_fork_and_gather, pin_digest]
+                pin_restore_roundtrip, pin_fork_and_gather, pin_digest, pin_append_history]
 
 
 # ------------------------------------------------------------- FP8 KV ----

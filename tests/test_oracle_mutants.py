@@ -54,6 +54,11 @@ MUTANTS = [
      "h *= 1099511628211ULL;", "h *= 1099511628213ULL;", "capsule"),
     ("gather_ignores_ids", "capsule_oracle.c",
      "gallery[ids[e]]);", "gallery[e % n_gallery]);", "capsule"),
+    ("append_window_keeps_oldest", "capsule_oracle.c",
+     "memcpy(dst, scratch + n * rb, (size_t)(W * rb));", "memcpy(dst, scratch, (size_t)(W * rb));", "capsule"),
+    ("append_positional_off_by_one", "capsule_oracle.c",
+     "memcpy(dst + position * rb, srcs[i], (size_t)(n * rb));",
+     "memcpy(dst + (position + 1) * rb, srcs[i], (size_t)((n - 1) * rb));", "capsule"),
     ("e4m3_bias_off_by_one", "fp8_oracle.c",
      "return ldexp(1.0 + (double)m / 8.0, (int)e - 7);", "return ldexp(1.0 + (double)m / 8.0, (int)e - 8);", "fp8"),
     ("e4m3_subnormal_scale", "fp8_oracle.c",

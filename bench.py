@@ -207,7 +207,8 @@ def main():
             else:
                 L = lays[li]
                 bufs.append(("lin%d.state" % li, L["state"], H * dk * dv * 4, 1, cap.CAP_KIND_FIXED))
-                bufs.append(("lin%d.conv" % li, L["conv"], L["conv"].numel(), 1, cap.CAP_KIND_FIXED))
+                # the conv tail: a window of conv_width rows of conv_channels bf16
+                bufs.append(("lin%d.conv" % li, L["conv"], w.conv_channels * 2, w.conv_width, cap.CAP_KIND_FIXED))
                 li += 1
         assert li == n_lin and ki == len(kvs)
         return bufs
@@ -224,12 +225,29 @@ def main():
         fk = [(n, torch.empty_like(t)) for n, t in kv]
         fork_keep.append((fl, fk))
         fork_sets.append(cap.cap_set_create(live_bufs(fl, fk), w.chunk, deploy))
+    # the continuation token's K/V rows and conv inputs (synthetic), one per buffer of the set
+    tok_src = []
+    for name, t, rb, rows, kind in bufs:
+        if name.endswith(".state"):
+            tok_src.append(None)
+        else:
+            x = torch.empty(rb, dtype=torch.uint8, device=dev)
+            x.view(torch.bfloat16).normal_(generator=torch.Generator(device=dev).manual_seed(len(tok_src)))
+            tok_src.append(x)
     flush = torch.empty(512 * 1024 * 1024, dtype=torch.uint8, device=dev)  # > MALL
     digest = cap.capsule_digest_tokens(synth.token_ids(w.seed, P))
     torch.cuda.synchronize()
     t_setup = time.perf_counter() - t_setup
 
     phases = ["scan_cs", "scan_final", "snapshot", "restore", "fork", "continue"]
+
+    def decode_token(strm):
+        """One continuation token: the K/V rows and conv inputs enter the set
+        (one append launch), then the 36 one-token recurrent updates."""
+        cap.cap_set_append(live, tok_src, 1, stream=strm)
+        for L in layers:
+            cap.linattn_chunked_prefill(L["q1"], L["k1"], L["v1"], L["g1"], L["o1"], state_in=L["state"],
+                                        final_state=L["state"], stream=strm)
 
     def step(record):
         ev = {k: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for k in phases}
@@ -260,9 +278,7 @@ def main():
             cap.capsule_fork(c, fork_sets, digest, stream=stream)
             ev["fork"][1].record(stream)
             ev["continue"][0].record(stream)
-            for L in layers:
-                cap.linattn_chunked_prefill(L["q1"], L["k1"], L["v1"], L["g1"], L["o1"], state_in=L["state"],
-                                            final_state=L["state"], stream=stream)
+            decode_token(stream)
             ev["continue"][1].record(stream)
         return ev, caps
 
@@ -281,11 +297,50 @@ def main():
     ms_per_step = wall * 1e3 / args.steps
 
     # post-run spot check: every fork branch holds the capsule's bytes (the
-    # set starts with lin0.state; KV is not touched by the continuation)
+    # set starts with lin0.state; the continuation appends K/V at row P, so
+    # rows [0, P) are the capsule's)
     nst = H * dk * dv * 4
     for fl, fk in fork_keep:
         assert torch.equal(fl[0]["state"].view(torch.uint8).flatten(), arena[:nst])
         assert torch.equal(fk[-1][1][: P * w.kv_row_bytes], kv[-1][1][: P * w.kv_row_bytes])
+
+    # ---- restore + one decode token as ONE HIP graph vs eager launches
+    # (outside the timed step; the graph is bound to this set, P and token)
+    c_g = recs[-1][1][0]
+    graph = torch.cuda.CUDAGraph()
+    stream.synchronize()
+    with torch.cuda.stream(stream):
+        with torch.cuda.graph(graph, stream=stream):
+            cap.capsule_restore(c_g, live, digest, stream=stream)
+            decode_token(stream)
+    dec_ms = {"eager": [], "graph": []}
+    enq_us = {"eager": [], "graph": []}
+    for rnd in range(6):
+        for mode in ("eager", "graph"):
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            with torch.cuda.stream(stream):
+                flush.fill_(rnd)
+                e[0].record(stream)
+                t_enq = time.perf_counter()
+                if mode == "graph":
+                    graph.replay()
+                else:
+                    cap.capsule_restore(c_g, live, digest, stream=stream)
+                    decode_token(stream)
+                t_enq = time.perf_counter() - t_enq
+                e[1].record(stream)
+            stream.synchronize()
+            if mode == "eager":
+                eager_state = layers[-1]["state"].clone()
+                eager_kv = kv[-1][1][P * w.kv_row_bytes:(P + 1) * w.kv_row_bytes].clone()
+            else:
+                assert torch.equal(layers[-1]["state"], eager_state)
+                assert torch.equal(kv[-1][1][P * w.kv_row_bytes:(P + 1) * w.kv_row_bytes], eager_kv)
+            if rnd:
+                dec_ms[mode].append(e[0].elapsed_time(e[1]))
+                enq_us[mode].append(t_enq * 1e6)
+    graph_ms, eager_ms = float(np.median(dec_ms["graph"])), float(np.median(dec_ms["eager"]))
+    del graph
 
     # ---- host tier, outside the timed step: demote the capsule to pinned
     # host memory and promote it back (each a stream-ordered copy over the
@@ -408,6 +463,11 @@ def main():
                       "link": "host link, PCIe 5.0 x16", "peak": LINK_PEAK_GBS, "unit": "GB/s",
                       "promote_frac": round(cap_bytes / (promote_ms * 1e-3) / 1e9 / LINK_PEAK_GBS, 4),
                       "capsule_ttft_ms_from_host": round(promote_ms + ms["restore"] + ms["continue"], 4)},
+        "restore_decode_graph": {"launches": 1 + 1 + n_lin, "eager_ms": round(eager_ms, 4),
+                                 "graph_ms": round(graph_ms, 4), "speedup": round(eager_ms / graph_ms, 3),
+                                 "host_enqueue_us": {"eager": round(float(np.median(enq_us["eager"])), 1),
+                                                     "graph": round(float(np.median(enq_us["graph"])), 1)},
+                                 "what": "capsule restore + one token (K/V + conv append, %d one-token scans)" % n_lin},
         "fp8_kv": {"capsule_bytes": cap8_bytes, "bf16_capsule_bytes": cap_bytes,
                    "restore_ms": round(f8ms["restore"], 4), "snapshot_ms": round(f8ms["snapshot"], 4),
                    "restore_gbs": round(2 * cap8_bytes / (f8ms["restore"] * 1e-3) / 1e9, 2),

@@ -131,6 +131,24 @@ CAP_API int cap_set_destroy(cap_set set);
 CAP_API int cap_set_set_position(cap_set set, uint64_t position);
 CAP_API int cap_set_get_position(cap_set set, uint64_t* position);
 
+/* Append a suffix of n tokens (§3 Algorithm 1 restore: "append suffix";
+ * §3 "Definition": positional KV region, fixed-size convolution window).
+ * srcs is a HOST array with one entry per buffer of the set, in set order:
+ * NULL leaves the buffer alone (e.g. a recurrent state, which the scan
+ * updates); otherwise a device pointer (16-byte aligned, disjoint from every
+ * live buffer) to n rows of that buffer's row_bytes:
+ *   positional buffer: rows [position, position + n) receive the n rows
+ *     (CAP_E_SIZE if position + n exceeds its rows);
+ *   fixed buffer: treated as a window of its `rows` rows holding the latest
+ *     rows of a history (a convolution tail [W, C] declared with row_bytes =
+ *     C * element size and rows = W); it becomes the last W rows of (its
+ *     rows, then the n new rows); at most 64 KiB per window
+ *     (CAP_E_UNSUPPORTED).
+ * One stream-ordered launch per 128 touched buffers; then the set's position
+ * advances by n.  The kernel arguments carry every address, so the call can
+ * be recorded in a stream capture (a HIP graph) and replayed. */
+CAP_API int cap_set_append(cap_set live, const void* const* srcs, uint64_t n, void* stream);
+
 /* Capsule bytes of this set at boundary P (P is aligned first). */
 CAP_API int capsule_bytes(cap_set set, uint64_t P, uint64_t* bytes);
 

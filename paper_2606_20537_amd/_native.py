@@ -67,6 +67,7 @@ SIGNATURES = [
     ("cap_set_destroy", ct.c_int, [_vp]),
     ("cap_set_set_position", ct.c_int, [_vp, _u64]),
     ("cap_set_get_position", ct.c_int, [_vp, ct.POINTER(_u64)]),
+    ("cap_set_append", ct.c_int, [_vp, ct.POINTER(_vp), _u64, _vp]),
     ("capsule_bytes", ct.c_int, [_vp, _u64, ct.POINTER(_u64)]),
     ("capsule_snapshot", ct.c_int, [_vp, _u64, _u64, _vp, _u64, _vp, ct.POINTER(_vp)]),
     ("capsule_restore", ct.c_int, [_vp, _vp, _u64, _vp, ct.POINTER(_u64)]),
@@ -214,6 +215,15 @@ def cap_set_get_position(s):
     out = _u64(0)
     _check("cap_set_get_position", load().cap_set_get_position(s.handle, ct.byref(out)))
     return int(out.value)
+
+
+def cap_set_append(s, srcs, n, stream=None):
+    """Append n tokens: srcs has one entry per buffer of the set (tensor,
+    address or None)."""
+    if len(srcs) != s.n:
+        raise ValueError("cap_set_append: %d sources for a set of %d buffers" % (len(srcs), s.n))
+    arr = (_vp * len(srcs))(*[None if x is None else _addr(x) for x in srcs])
+    return _check("cap_set_append", load().cap_set_append(s.handle, arr, int(n), _stream(stream)))
 
 
 def capsule_bytes(s, P):

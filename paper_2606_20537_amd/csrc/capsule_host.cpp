@@ -466,6 +466,59 @@ int capsule_release(cap_capsule cap) {
     return CAP_OK;
 }
 
+// ------------------------------------------------------------ append ----
+int cap_set_append(cap_set live, const void* const* srcs, uint64_t n, void* stream) {
+    if (!live || !srcs) return CAP_E_INVAL;
+    const uint32_t nb = (uint32_t)live->bufs.size();
+    std::vector<uint32_t> idx;
+    for (uint32_t i = 0; i < nb; ++i) {
+        if (!srcs[i]) continue;
+        const BufInfo& b = live->bufs[i];
+        if (!aligned16((uint64_t)(uintptr_t)srcs[i])) return CAP_E_ALIGN;
+        if (n > UINT64_MAX / b.row_bytes) return CAP_E_SIZE;
+        if (b.kind == CAP_KIND_POSITIONAL) {
+            if (live->position > b.rows || n > b.rows - live->position) return CAP_E_SIZE;
+        } else if (b.row_bytes * b.rows > cap::kAppendMaxWindow) {
+            return CAP_E_UNSUPPORTED;
+        }
+        const uint64_t s0 = (uint64_t)(uintptr_t)srcs[i], s1 = s0 + n * b.row_bytes;
+        for (const BufInfo& o : live->bufs)
+            if (overlaps(s0, s1, o.ptr, o.ptr + o.row_bytes * o.rows)) return CAP_E_INVAL;
+        idx.push_back(i);
+    }
+    int rc = current_device_matches(live);
+    if (rc != CAP_OK) return rc;
+    if (n > 0) {
+        for (size_t first = 0; first < idx.size(); first += cap::kAppendMaxSeg) {
+            const size_t cnt = std::min<size_t>(cap::kAppendMaxSeg, idx.size() - first);
+            cap::AppendParams p{};
+            uint64_t blocks = 0;
+            for (size_t k = 0; k < cnt; ++k) {
+                const BufInfo& b = live->bufs[idx[first + k]];
+                p.src[k] = (uint64_t)(uintptr_t)srcs[idx[first + k]];
+                p.bytes[k] = n * b.row_bytes;
+                p.first_block[k] = (uint32_t)blocks;
+                if (b.kind == CAP_KIND_POSITIONAL) {
+                    p.dst[k] = b.ptr + live->position * b.row_bytes;
+                    p.win[k] = 0;
+                    blocks += (p.bytes[k] + cap::kAppendTile - 1) / cap::kAppendTile;
+                } else {
+                    p.dst[k] = b.ptr;
+                    p.win[k] = (uint32_t)(b.row_bytes * b.rows);
+                    blocks += 1;
+                }
+                if (blocks > 0x7fffffffull) return CAP_E_SIZE;
+            }
+            p.first_block[cnt] = (uint32_t)blocks;
+            p.n_seg = (uint32_t)cnt;
+            rc = launch_status(cap::launch_append(p, static_cast<hipStream_t>(stream)));
+            if (rc != CAP_OK) return rc;
+        }
+    }
+    live->position += n;
+    return CAP_OK;
+}
+
 // ------------------------------------------------------------ FP8 KV ----
 static int fp8_convert(const kv_fp8_seg* segs, uint32_t n_seg, void* stream, bool quantize) {
     if (!segs || n_seg == 0) return CAP_E_INVAL;

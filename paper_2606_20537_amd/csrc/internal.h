@@ -1,5 +1,5 @@
 // Internal interface between the host ABI (capsule_host.cpp) and the HIP
-// kernels (capsule_copy.hip, linattn_scan.hip, kv_fp8.hip).  Not part of the
+// kernels (capsule_copy.hip, linattn_scan.hip, kv_fp8.hip, append.hip).  Not part of the
 // public ABI.
 #pragma once
 
@@ -86,5 +86,27 @@ struct Fp8Params {
 };
 
 hipError_t launch_fp8(const Fp8Params& p, hipStream_t stream);
+
+// Append of a suffix of n tokens to a live set (one launch, up to
+// kAppendMaxSeg buffers).  Segment s is either a positional copy of
+// bytes[s] bytes from src[s] to dst[s] (tiles of kAppendTile bytes, several
+// blocks), or, when win[s] != 0, a sliding window of win[s] bytes at dst[s]
+// that takes the last win[s] bytes of (window, then the bytes[s] source
+// bytes) in one block.  Block b works on segment s with first_block[s] <= b
+// < first_block[s + 1].
+constexpr int kAppendMaxSeg = 128;
+constexpr uint32_t kAppendTile = 16384;        // bytes per positional block
+constexpr uint32_t kAppendMaxWindow = 65536;   // bytes of one window
+
+struct AppendParams {
+    uint64_t src[kAppendMaxSeg];
+    uint64_t dst[kAppendMaxSeg];
+    uint64_t bytes[kAppendMaxSeg];
+    uint32_t win[kAppendMaxSeg];
+    uint32_t first_block[kAppendMaxSeg + 1];
+    uint32_t n_seg;
+};
+
+hipError_t launch_append(const AppendParams& p, hipStream_t stream);
 
 }  // namespace cap

@@ -10,7 +10,8 @@ live state in place; snapshot / restore / fork go through the capsule calls.
 What the out-of-scope parts of a model would produce is replaced by seeded
 synthetic tables (synth): the per-token q/k/v/g of each linear layer, the K/V
 rows each full-attention layer appends, and the conv inputs whose last W rows
-form the tail.  Appending those rows is plain tensor copying in this harness.
+form the tail.  Those rows enter the live set through the library's append
+(cap_set_append: positional K/V rows, sliding conv windows).
 """
 import numpy as np
 import torch
@@ -50,8 +51,8 @@ class HybridStack:
                     ki += 1
             else:
                 bufs.append(("state%d" % li, self.state[li], H * dk * dv * 4, 1, cap.CAP_KIND_FIXED))
-                c = self.conv[li]
-                bufs.append(("conv%d" % li, c, c.numel() * 2, 1, cap.CAP_KIND_FIXED))
+                c = self.conv[li]  # a window of W rows of C bf16
+                bufs.append(("conv%d" % li, c, c.shape[1] * 2, c.shape[0], cap.CAP_KIND_FIXED))
                 li += 1
         self.bufs = bufs
         self.set = cap.cap_set_create(bufs, w.chunk, deploy_key)
@@ -59,14 +60,19 @@ class HybridStack:
 
     # --- the model's other layers, replaced by synthetic tables -----------
     def _append_rows(self, t0, t1):
-        for i, kvt in enumerate(self.kv):
-            kvt[t0:t1].copy_(self.inp["kv"][i][t0:t1])
-        cw = self.w.conv_width
-        if cw:
-            for l in range(self.w.n_linear):
-                src = self.inp["conv"][l]
-                rows = [src[t] if t >= 0 else torch.zeros_like(src[0]) for t in range(t1 - cw, t1)]
-                self.conv[l].copy_(torch.stack(rows))
+        """The K/V rows and conv inputs of tokens [t0, t1) enter the set
+        (one cap_set_append launch; the states are the scan's)."""
+        srcs, ki, li = [], 0, 0
+        for name, t, rb, rows, kind in self.bufs:
+            if name.startswith("kv"):
+                srcs.append(self.inp["kv"][ki][t0:t1])
+                ki += 1
+            elif name.startswith("conv"):
+                srcs.append(self.inp["conv"][li][t0:t1] if self.w.conv_width else None)
+                li += 1
+            else:
+                srcs.append(None)
+        cap.cap_set_append(self.set, srcs, t1 - t0)
 
     # --- the hot path -----------------------------------------------------
     def prefill(self, t0, t1):
@@ -80,9 +86,9 @@ class HybridStack:
                                         self.o[l][t0:t1], state_in=self.state[l], final_state=self.state[l],
                                         T=T, H=w.heads, dk=w.dk, dv=w.dv, chunk=w.chunk,
                                         in_dtype=cap.CAP_DTYPE_F32 if w.in_dtype == "f32" else cap.CAP_DTYPE_BF16)
+        cap.cap_set_set_position(self.set, t0)
         self._append_rows(t0, t1)
         self.pos = t1
-        cap.cap_set_set_position(self.set, t1)
 
     def decode(self, n):
         for _ in range(n):

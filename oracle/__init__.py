@@ -54,6 +54,10 @@ class Oracle:
         L.orc_digest_tokens.restype = u64
         L.orc_digest_bytes.argtypes = [vp, u64]
         L.orc_digest_bytes.restype = u64
+        L.orc_gdn_sequential.argtypes = [i64, i64, i64, i64, vp, vp, vp, vp, vp, ct.c_double, vp, vp, vp]
+        L.orc_gdn_sequential.restype = ct.c_int
+        L.orc_gdn_chunked.argtypes = [i64, i64, i64, i64, i64, vp, vp, vp, vp, vp, ct.c_double, vp, vp, vp, vp]
+        L.orc_gdn_chunked.restype = ct.c_int
         L.orc_e4m3_decode.argtypes = [ct.c_uint8]
         L.orc_e4m3_decode.restype = ct.c_float
         L.orc_e4m3_encode.argtypes = [ct.c_float]
@@ -106,6 +110,40 @@ class Oracle:
                                           float(scale), _ptr(S0), _ptr(o), _ptr(cs), _ptr(S))
         if rc != 0:
             raise ValueError("orc_linattn_chunked failed")
+        return o, cs, S
+
+    # ---- gated delta rule (the model's Gated DeltaNet state; reading in gdn_oracle.c) ----
+    def _gdn_check(self, q, k, v, g, beta):
+        T, H, dk, dv = self._check_inputs(q, k, v, g)
+        if not (isinstance(beta, np.ndarray) and beta.dtype == np.float32 and beta.flags.c_contiguous
+                and beta.shape == (T, H)):
+            raise ValueError("beta must be a C-contiguous float32 [T, H] array")
+        return T, H, dk, dv
+
+    def gdn_sequential(self, q, k, v, g, beta, S0=None, scale=1.0):
+        """S_t = exp(g_t)(I - beta_t k_t^T k_t) S_{t-1} + beta_t k_t^T v_t, o_t = scale q_t S_t,
+        token by token.  Returns (o [T,H,dv] f64, S_final [H,dk,dv] f64)."""
+        T, H, dk, dv = self._gdn_check(q, k, v, g, beta)
+        S0 = None if S0 is None else np.ascontiguousarray(S0, dtype=np.float64)
+        o = np.empty((T, H, dv), np.float64)
+        S = np.empty((H, dk, dv), np.float64)
+        if self.lib.orc_gdn_sequential(T, H, dk, dv, _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), float(scale),
+                                       _ptr(S0), _ptr(o), _ptr(S)) != 0:
+            raise ValueError("orc_gdn_sequential failed")
+        return o, S
+
+    def gdn_chunked(self, q, k, v, g, beta, chunk, S0=None, scale=1.0):
+        """The chunked (WY) form with chunk size ``chunk``.  Returns
+        (o, chunk_states [ceil(T/C),H,dk,dv] (state entering each chunk), S_final), fp64."""
+        T, H, dk, dv = self._gdn_check(q, k, v, g, beta)
+        S0 = None if S0 is None else np.ascontiguousarray(S0, dtype=np.float64)
+        n_chunks = (T + chunk - 1) // chunk
+        o = np.empty((T, H, dv), np.float64)
+        cs = np.empty((n_chunks, H, dk, dv), np.float64)
+        S = np.empty((H, dk, dv), np.float64)
+        if self.lib.orc_gdn_chunked(T, H, dk, dv, int(chunk), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta),
+                                    float(scale), _ptr(S0), _ptr(o), _ptr(cs), _ptr(S)) != 0:
+            raise ValueError("orc_gdn_chunked failed")
         return o, cs, S
 
     # ---- capsule verbs as memcpy (§3 Algorithm 1, "Four verbs") ----

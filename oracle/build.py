@@ -9,7 +9,7 @@ import subprocess
 import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-SOURCES = ["linattn_oracle.c", "capsule_oracle.c", "fp8_oracle.c"]
+SOURCES = ["linattn_oracle.c", "capsule_oracle.c", "fp8_oracle.c", "gdn_oracle.c"]
 LIB_PATH = os.path.join(HERE, "_build", "liborc.so")
 
 

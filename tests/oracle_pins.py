@@ -517,7 +517,101 @@ def pin_fp8_arrays_scale_and_bf16(orc):
         assert orc.bf16_round(y) == w, (float(y), orc.bf16_round(y), int(w))
 
 
+# ------------------------------------------------------- gated delta rule ----
+def _gdn_inputs(seed, T, H, dk, dv, g_lo=-0.3):
+    r = rng(seed, 0, "gdnpin")
+    q = r.standard_normal((T, H, dk)).astype(np.float32)
+    k = r.standard_normal((T, H, dk))
+    k = (k / np.linalg.norm(k, axis=-1, keepdims=True)).astype(np.float32)
+    v = r.standard_normal((T, H, dv)).astype(np.float32)
+    g = r.uniform(g_lo, 0.0, (T, H)).astype(np.float32)
+    beta = r.uniform(0.0, 1.0, (T, H)).astype(np.float32)
+    S0 = r.standard_normal((H, dk, dv))
+    return q, k, v, g, beta, S0
+
+
+def pin_gdn_chunked_equals_sequential(orc):
+    """Two algorithms: the chunked WY form equals the recurrence (any chunk
+    size, ragged tail, entering state), and its chunk states are the
+    recurrence's states at the chunk starts."""
+    q, k, v, g, b, S0 = _gdn_inputs(1, 150, 2, 16, 8)
+    o1, s1 = orc.gdn_sequential(q, k, v, g, b, S0, scale=0.5)
+    for C in (1, 7, 64):
+        o2, cs, s2 = orc.gdn_chunked(q, k, v, g, b, C, S0, scale=0.5)
+        assert _rel(o2, o1) < 1e-11 and _rel(s2, s1) < 1e-11, C
+        for j in range(1, cs.shape[0]):
+            _, sj = orc.gdn_sequential(q[: j * C], k[: j * C], v[: j * C], g[: j * C], b[: j * C], S0)
+            assert _rel(cs[j], sj) < 1e-11, (C, j)
+
+
+def pin_gdn_beta_zero_is_pure_decay(orc):
+    """beta = 0 writes nothing: S_t = exp(G_t) S0, o_t = exp(G_t) q_t S0."""
+    q, k, v, g, b, S0 = _gdn_inputs(2, 70, 2, 8, 4, g_lo=-1.0)
+    b[:] = 0.0
+    G = np.cumsum(g.astype(np.float64), axis=0)
+    want_o = np.exp(G)[:, :, None] * np.einsum("thd,hde->the", q.astype(np.float64), S0)
+    for o, S in (orc.gdn_sequential(q, k, v, g, b, S0), orc.gdn_chunked(q, k, v, g, b, 16, S0)[::2]):
+        assert _rel(o, want_o) < 1e-12
+        assert _rel(S, np.exp(G[-1])[:, None, None] * S0) < 1e-12
+
+
+def pin_gdn_orthonormal_keys_store_values(orc):
+    """With orthonormal keys and beta = 1 the delta rule stores each value
+    exactly under its key: right after token t, k_t S_t = v_t; an earlier key
+    reads its value decayed by the gates since, k_i S_t = exp(G_t - G_i) v_i;
+    directions orthogonal to every key keep exp(G_t) S0."""
+    r = rng(3, 0, "gdnpin")
+    dk, dv, n = 16, 5, 6
+    Hm = np.array([[1.0]])
+    while Hm.shape[0] < dk:                            # Sylvester's Hadamard matrix
+        Hm = np.block([[Hm, Hm], [Hm, -Hm]])
+    Qm = Hm[r.permutation(dk)] / 4.0                   # orthonormal rows, exact in fp32
+    keys = Qm[:n].astype(np.float32)
+    free = Qm[n:]                                      # their complement
+    k = keys[:, None, :]
+    v = r.standard_normal((n, 1, dv)).astype(np.float32)
+    g = r.uniform(-0.5, 0.0, (n, 1)).astype(np.float32)
+    b = np.ones((n, 1), np.float32)
+    S0 = r.standard_normal((1, dk, dv))
+    G = np.cumsum(g[:, 0].astype(np.float64))
+    kd = keys.astype(np.float64)
+    for t in range(n):
+        for fn in (lambda T: orc.gdn_sequential(k[:T], k[:T], v[:T], g[:T], b[:T], S0)[1],
+                   lambda T: orc.gdn_chunked(k[:T], k[:T], v[:T], g[:T], b[:T], 4, S0)[2]):
+            S = fn(t + 1)[0]
+            for i in range(t + 1):
+                want = np.exp(G[t] - G[i]) * v[i, 0].astype(np.float64)
+                assert np.abs(kd[i] @ S - want).max() < 1e-9, (t, i)
+            assert np.abs(free @ S - np.exp(G[t]) * (free @ S0[0])).max() < 1e-9
+
+
+def pin_gdn_linearity_and_causality(orc):
+    """(o, S) is linear in (v, S0) jointly for fixed q, k, g, beta; outputs
+    before a token do not depend on it or anything after it."""
+    q, k, v1, g, b, S1 = _gdn_inputs(4, 90, 1, 8, 4)
+    _, _, v2, _, _, S2 = _gdn_inputs(5, 90, 1, 8, 4)
+    o1, s1 = orc.gdn_chunked(q, k, v1, g, b, 32, S1)[::2]
+    o2, s2 = orc.gdn_chunked(q, k, v2, g, b, 32, S2)[::2]
+    v3 = (2.0 * v1.astype(np.float64) - 3.0 * v2.astype(np.float64)).astype(np.float32)
+    o3, s3 = orc.gdn_chunked(q, k, v3, g, b, 32, 2.0 * S1 - 3.0 * S2)[::2]
+    dv_err = (v3.astype(np.float64) - (2.0 * v1.astype(np.float64) - 3.0 * v2.astype(np.float64)))
+    assert np.abs(dv_err).max() < 1e-5  # v3 is the fp32 rounding of the combination
+    o12, s12 = orc.gdn_sequential(q, k, v3, g, b, 2.0 * S1 - 3.0 * S2)
+    assert _rel(o3, o12) < 1e-11 and _rel(s3, s12) < 1e-11
+    oL = 2.0 * o1 - 3.0 * o2
+    assert _rel(o3, oL) < 1e-5 and _rel(s3, 2.0 * s1 - 3.0 * s2) < 1e-5
+    cut = 50
+    k2, v4 = k.copy(), v1.copy()
+    k2[cut:] = np.roll(k2[cut:], 1, axis=-1)
+    v4[cut:] *= -2.0
+    o4 = orc.gdn_chunked(q, k2, v4, g, b, 32, S1)[0]
+    assert np.array_equal(o4[:cut], o1[:cut]) and not np.allclose(o4[cut:], o1[cut:])
+
+
+GDN_PINS = [pin_gdn_chunked_equals_sequential, pin_gdn_beta_zero_is_pure_decay,
+            pin_gdn_orthonormal_keys_store_values, pin_gdn_linearity_and_causality]
+
 FP8_PINS = [pin_e4m3_published_values, pin_e4m3_against_torch, pin_e4m3_round_trip_and_saturation,
             pin_fp8_arrays_scale_and_bf16]
 
-ALL_PINS = SCAN_PINS + CAPSULE_PINS + FP8_PINS
+ALL_PINS = SCAN_PINS + CAPSULE_PINS + FP8_PINS + GDN_PINS

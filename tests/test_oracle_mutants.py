@@ -13,7 +13,7 @@ import pytest
 
 import oracle
 from oracle import build as obuild
-from oracle_pins import CAPSULE_PINS, FP8_PINS, SCAN_PINS
+from oracle_pins import CAPSULE_PINS, FP8_PINS, GDN_PINS, SCAN_PINS
 
 ORACLE_DIR = os.path.dirname(os.path.abspath(oracle.__file__))
 
@@ -59,6 +59,23 @@ MUTANTS = [
     ("append_positional_off_by_one", "capsule_oracle.c",
      "memcpy(dst + position * rb, srcs[i], (size_t)(n * rb));",
      "memcpy(dst + (position + 1) * rb, srcs[i], (size_t)((n - 1) * rb));", "capsule"),
+    ("gdn_seq_correction_sign", "gdn_oracle.c",
+     "a * (S[i * dv + j] - b * ki * kS[j])", "a * (S[i * dv + j] + b * ki * kS[j])", "gdn"),
+    ("gdn_seq_correction_without_beta", "gdn_oracle.c",
+     "a * (S[i * dv + j] - b * ki * kS[j])", "a * (S[i * dv + j] - ki * kS[j])", "gdn"),
+    ("gdn_seq_decay_after_correction", "gdn_oracle.c",
+     "a * (S[i * dv + j] - b * ki * kS[j])", "a * S[i * dv + j] - b * ki * kS[j]", "gdn"),
+    ("gdn_chunk_solve_sign", "gdn_oracle.c",
+     "for (int64_t j = 0; j < t; ++j) acc -= A[t * C + j] * W[j * dk + d];",
+     "for (int64_t j = 0; j < t; ++j) acc += A[t * C + j] * W[j * dk + d];", "gdn"),
+    ("gdn_chunk_w_without_gamma", "gdn_oracle.c",
+     "double acc = bt * gt * (double)AT3(k, t0 + t, h, d, H, dk);",
+     "double acc = bt * (double)AT3(k, t0 + t, h, d, H, dk);", "gdn"),
+    ("gdn_chunk_mask_drops_diagonal", "gdn_oracle.c",
+     "for (int64_t j = 0; j <= t; ++j) {", "for (int64_t j = 0; j < t; ++j) {", "gdn"),
+    ("gdn_chunk_fold_weight_dropped", "gdn_oracle.c",
+     "acc += exp(G[L - 1] - G[j]) * (double)AT3(k, t0 + j, h, d, H, dk) * U[j * dv + e];",
+     "acc += (double)AT3(k, t0 + j, h, d, H, dk) * U[j * dv + e];", "gdn"),
     ("e4m3_bias_off_by_one", "fp8_oracle.c",
      "return ldexp(1.0 + (double)m / 8.0, (int)e - 7);", "return ldexp(1.0 + (double)m / 8.0, (int)e - 8);", "fp8"),
     ("e4m3_subnormal_scale", "fp8_oracle.c",
@@ -87,7 +104,7 @@ def test_mutant_is_caught(tmp_path, mid, fname, old, new, family):
     (src / fname).write_text(text.replace(old, new))
     lib = obuild.build(out_path=str(tmp_path / ("liborc_%s.so" % mid)), src_dir=str(src))
     mutant = oracle.Oracle(lib)
-    pins = {"scan": SCAN_PINS, "capsule": CAPSULE_PINS, "fp8": FP8_PINS}[family]
+    pins = {"scan": SCAN_PINS, "capsule": CAPSULE_PINS, "fp8": FP8_PINS, "gdn": GDN_PINS}[family]
     caught = []
     for pin in pins:
         try:

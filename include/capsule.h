@@ -275,6 +275,62 @@ typedef struct linattn_args {
 
 CAP_API int linattn_chunked_prefill(const linattn_args* args, void* stream);
 
+/* -------------------------------------- chunked gated delta-rule prefill -- */
+/* Gated DeltaNet state of the paper's hybrid model (§2 "hybrid recurrent
+ * state", §7 model description; the paper does not write the recurrence,
+ * the standard gated delta rule is taken), per head h with state dk x dv:
+ *     S_t = exp(g_t) (I - beta_t k_t^T k_t) S_{t-1} + beta_t k_t^T v_t
+ *     o_t = scale * q_t S_t
+ * computed in chunks of C tokens counted from the first token of the call.
+ * For a chunk with entering state S and inclusive in-chunk log-decay sums
+ * G_t (gamma_t = exp(G_t)) the pseudo-values U solve
+ *     (I + A) U = diag(beta) (V - diag(gamma) K S),
+ *     A_tm = beta_t exp(G_t - G_m) (k_t . k_m)  for m < t,
+ * and o_t = scale (gamma_t q_t S + sum_{m<=t} exp(G_t - G_m)(q_t . k_m) u_m),
+ * S_new = gamma_last S + sum_m exp(G_last - G_m) k_m^T u_m.  As for the
+ * linear-attention scan, a chunk's arithmetic depends only on (S, that
+ * chunk's inputs): restore at an aligned position then continue equals one
+ * longer call bit for bit.
+ *
+ * Layouts (contiguous, device, caller-owned):
+ *   q, k : [T, H, dk] bf16     v : [T, H, dv] bf16
+ *   g    : [T, H] fp32 log-gates, finite (normally <= 0)
+ *   beta : [T, H] fp32 write strengths (normally in [0, 1])
+ *   state_in, chunk_states, final_state, o : as in linattn_args
+ *   workspace : gdn_workspace_bytes(T, H, C) bytes of device scratch, 16-byte
+ *               aligned; holds the per-chunk inverses (I + A)^-1 during the
+ *               call (contents undefined afterwards).  May be NULL when T = 0.
+ * Supported: chunk == 64, dk in {64, 128}, dv a multiple of 16, bf16 inputs.
+ * Errors: CAP_E_INVAL (null required pointer, T < 0, H < 1, bad dtype,
+ * overlapping buffers), CAP_E_SIZE (workspace_bytes too small),
+ * CAP_E_UNSUPPORTED (shape outside the list), CAP_E_ALIGN. */
+typedef struct gdn_args {
+    const void*  q;
+    const void*  k;
+    const void*  v;
+    const float* g;
+    const float* beta;
+    const float* state_in;
+    float*       o;
+    float*       chunk_states;
+    float*       final_state;
+    void*        workspace;
+    uint64_t     workspace_bytes;
+    int64_t      T;
+    int32_t      H;
+    int32_t      dk;
+    int32_t      dv;
+    int32_t      chunk;
+    int32_t      in_dtype;   /* CAP_DTYPE_BF16 */
+    float        scale;
+} gdn_args;
+
+/* Workspace size for gdn_chunked_prefill: ceil(T / chunk) * H * chunk^2 * 4
+ * bytes (0 for T <= 0, H < 1 or chunk < 1). */
+CAP_API uint64_t gdn_workspace_bytes(int64_t T, int32_t H, int32_t chunk);
+
+CAP_API int gdn_chunked_prefill(const gdn_args* args, void* stream);
+
 /* ---------------------------------------------------------- FP8 KV ------ */
 /* §3 "Definition": the KV region may be held in FP8, which roughly halves
  * the capsule (an FP8 K or V buffer is an ordinary POSITIONAL buffer with

@@ -1,5 +1,5 @@
-"""Execution-state capsules and the chunked gated linear-attention prefill
-scan for AMD Instinct MI355X (gfx950).
+"""Execution-state capsules and the chunked gated linear-attention and gated
+delta-rule prefill scans for AMD Instinct MI355X (gfx950).
 
 The product is libcapsule.so (C ABI, include/capsule.h; HIP kernels under
 csrc/).  This package holds its build script and a ctypes binding whose
@@ -11,6 +11,6 @@ from ._native import (  # noqa: F401
     CAP_MAX_GALLERY, CAP_OK, CAP_TIER_DEVICE, CAP_TIER_HOST, SIGNATURES, CapSet, Capsule, CapsuleError, cap_align_boundary, cap_set_append, cap_set_create,
     cap_set_destroy, cap_set_get_position, cap_set_set_position, cap_status_string, capsule_bytes,
     capsule_digest_tokens, capsule_fork, capsule_gather_restore, capsule_info, capsule_layout_bytes,
-    capsule_move, capsule_release, capsule_restore, capsule_snapshot, capsule_tier, kv_fp8_dequantize, kv_fp8_quantize,
-    linattn_chunked_prefill, load,
+    capsule_move, capsule_release, capsule_restore, capsule_snapshot, capsule_tier, gdn_chunked_prefill,
+    gdn_workspace_bytes, kv_fp8_dequantize, kv_fp8_quantize, linattn_chunked_prefill, load,
 )

@@ -52,6 +52,14 @@ class linattn_args(ct.Structure):
                 ("dv", ct.c_int32), ("chunk", ct.c_int32), ("in_dtype", ct.c_int32), ("scale", ct.c_float)]
 
 
+class gdn_args(ct.Structure):
+    _fields_ = [("q", ct.c_void_p), ("k", ct.c_void_p), ("v", ct.c_void_p), ("g", ct.c_void_p),
+                ("beta", ct.c_void_p), ("state_in", ct.c_void_p), ("o", ct.c_void_p),
+                ("chunk_states", ct.c_void_p), ("final_state", ct.c_void_p), ("workspace", ct.c_void_p),
+                ("workspace_bytes", ct.c_uint64), ("T", ct.c_int64), ("H", ct.c_int32), ("dk", ct.c_int32),
+                ("dv", ct.c_int32), ("chunk", ct.c_int32), ("in_dtype", ct.c_int32), ("scale", ct.c_float)]
+
+
 class kv_fp8_seg(ct.Structure):
     _fields_ = [("src", ct.c_void_p), ("dst", ct.c_void_p), ("n", ct.c_uint64), ("scale", ct.c_float),
                 ("reserved", ct.c_uint32)]
@@ -82,6 +90,8 @@ SIGNATURES = [
     ("capsule_release", ct.c_int, [_vp]),
     ("capsule_digest_tokens", _u64, [ct.POINTER(_i32), _u64]),
     ("linattn_chunked_prefill", ct.c_int, [ct.POINTER(linattn_args), _vp]),
+    ("gdn_workspace_bytes", _u64, [ct.c_int64, _i32, _i32]),
+    ("gdn_chunked_prefill", ct.c_int, [ct.POINTER(gdn_args), _vp]),
 ]
 
 _lib = None
@@ -311,6 +321,34 @@ def linattn_chunked_prefill(q, k, v, g, o, *, state_in=None, chunk_states=None, 
     a = linattn_args(_addr(q), _addr(k), _addr(v), _addr(g), _addr(state_in), _addr(o), _addr(chunk_states),
                      _addr(final_state), int(T), int(H), int(dk), int(dv), int(chunk), int(in_dtype), float(scale))
     return _check("linattn_chunked_prefill", load().linattn_chunked_prefill(ct.byref(a), _stream(stream)))
+
+
+def gdn_workspace_bytes(T, H, chunk=64):
+    """Bytes of device workspace gdn_chunked_prefill needs for T tokens, H heads."""
+    return int(load().gdn_workspace_bytes(int(T), int(H), int(chunk)))
+
+
+def gdn_chunked_prefill(q, k, v, g, beta, o, *, state_in=None, chunk_states=None, final_state=None,
+                        workspace=None, workspace_bytes=None, T=None, H=None, dk=None, dv=None, chunk=64,
+                        in_dtype=CAP_DTYPE_BF16, scale=1.0, stream=None):
+    """Marshal tensors (or addresses with explicit sizes) into gdn_args.
+
+    With no workspace given, one is allocated as a torch uint8 tensor on q's
+    device for the duration of the call (stream-ordered by torch's caching
+    allocator)."""
+    if T is None:
+        T, H, dk = q.shape
+        dv = v.shape[2]
+    need = gdn_workspace_bytes(T, H, chunk) if chunk > 0 and H > 0 else 0
+    if workspace is None and need > 0:
+        import torch
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    if workspace_bytes is None:
+        workspace_bytes = workspace.numel() * workspace.element_size() if hasattr(workspace, "numel") else need
+    a = gdn_args(_addr(q), _addr(k), _addr(v), _addr(g), _addr(beta), _addr(state_in), _addr(o),
+                 _addr(chunk_states), _addr(final_state), _addr(workspace), int(workspace_bytes), int(T), int(H),
+                 int(dk), int(dv), int(chunk), int(in_dtype), float(scale))
+    return _check("gdn_chunked_prefill", load().gdn_chunked_prefill(ct.byref(a), _stream(stream)))
 
 
 def _fp8_segs(segs):

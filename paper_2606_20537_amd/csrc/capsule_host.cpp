@@ -624,4 +624,61 @@ int linattn_chunked_prefill(const linattn_args* a, void* stream) {
     return launch_status(cap::launch_linattn_scan(p, static_cast<hipStream_t>(stream)));
 }
 
+uint64_t gdn_workspace_bytes(int64_t T, int32_t H, int32_t chunk) {
+    if (T <= 0 || H < 1 || chunk < 1) return 0;
+    const uint64_t n = ((uint64_t)T + (uint64_t)chunk - 1) / (uint64_t)chunk;
+    return n * (uint64_t)H * (uint64_t)chunk * (uint64_t)chunk * 4u;
+}
+
+int gdn_chunked_prefill(const gdn_args* a, void* stream) {
+    if (!a) return CAP_E_INVAL;
+    if (a->T < 0 || a->H < 1 || a->dk < 1 || a->dv < 1 || a->chunk < 1) return CAP_E_INVAL;
+    if (a->in_dtype != CAP_DTYPE_BF16 && a->in_dtype != CAP_DTYPE_F32) return CAP_E_INVAL;
+    if (a->in_dtype != CAP_DTYPE_BF16) return CAP_E_UNSUPPORTED;
+    if (a->chunk != 64 || (a->dk != 64 && a->dk != 128) || (a->dv % 16) != 0) return CAP_E_UNSUPPORTED;
+    // 32-bit offsets inside one chunk of q / k / v / o rows, and grid sizes
+    const uint64_t T = (uint64_t)a->T, H = (uint64_t)a->H, dk = (uint64_t)a->dk, dv = (uint64_t)a->dv;
+    const uint64_t nck = (T + 63) / 64;
+    if (64 * H * (dk > dv ? dk : dv) * 4 > 0x7fffffffull) return CAP_E_UNSUPPORTED;
+    if (H * (dv / 16) > 0x7fffffffull || nck * H > 0x7fffffffull) return CAP_E_UNSUPPORTED;
+    if (a->T > 0 && (!a->q || !a->k || !a->v || !a->g || !a->beta || !a->o || !a->workspace)) return CAP_E_INVAL;
+    const uint64_t ws_need = gdn_workspace_bytes(a->T, a->H, a->chunk);
+    if (a->T > 0 && a->workspace_bytes < ws_need) return CAP_E_SIZE;
+    const uint64_t ptrs[] = {(uint64_t)(uintptr_t)a->q, (uint64_t)(uintptr_t)a->k, (uint64_t)(uintptr_t)a->v,
+                             (uint64_t)(uintptr_t)a->g, (uint64_t)(uintptr_t)a->beta,
+                             (uint64_t)(uintptr_t)a->state_in, (uint64_t)(uintptr_t)a->o,
+                             (uint64_t)(uintptr_t)a->chunk_states, (uint64_t)(uintptr_t)a->final_state,
+                             (uint64_t)(uintptr_t)a->workspace};
+    for (uint64_t p : ptrs)
+        if (!aligned16(p)) return CAP_E_ALIGN;
+    // outputs (and the workspace) must not overlap the inputs or each other;
+    // final_state may alias state_in
+    struct R { uint64_t p, n; };
+    const R in[] = {{ptrs[0], T * H * dk * 2}, {ptrs[1], T * H * dk * 2}, {ptrs[2], T * H * dv * 2},
+                    {ptrs[3], T * H * 4}, {ptrs[4], T * H * 4}, {ptrs[5], H * dk * dv * 4}};
+    const R outr[] = {{ptrs[6], T * H * dv * 4}, {ptrs[7], nck * H * dk * dv * 4}, {ptrs[8], H * dk * dv * 4},
+                      {ptrs[9], T > 0 ? ws_need : 0}};
+    constexpr int NIN = sizeof(in) / sizeof(in[0]), NOUT = sizeof(outr) / sizeof(outr[0]);
+    for (int i = 0; i < NOUT; ++i) {
+        if (!outr[i].p || !outr[i].n) continue;
+        for (int j = 0; j < NIN; ++j) {
+            if (!in[j].p || !in[j].n) continue;
+            if (i == 2 && j == 5 && outr[i].p == in[j].p) continue;  // in-place state update
+            if (overlaps(outr[i].p, outr[i].p + outr[i].n, in[j].p, in[j].p + in[j].n)) return CAP_E_INVAL;
+        }
+        for (int j = 0; j < i; ++j) {
+            if (!outr[j].p || !outr[j].n) continue;
+            if (overlaps(outr[i].p, outr[i].p + outr[i].n, outr[j].p, outr[j].p + outr[j].n)) return CAP_E_INVAL;
+        }
+    }
+    cap::GdnParams p{};
+    p.q = a->q; p.k = a->k; p.v = a->v; p.g = a->g; p.beta = a->beta;
+    p.state_in = a->state_in; p.o = a->o; p.chunk_states = a->chunk_states; p.final_state = a->final_state;
+    p.ws = static_cast<float*>(a->workspace);
+    p.T = a->T; p.H = a->H; p.dk = a->dk; p.dv = a->dv;
+    p.scale = a->scale;
+    if (a->T == 0 && !a->final_state) return CAP_OK;
+    return launch_status(cap::launch_gdn(p, static_cast<hipStream_t>(stream)));
+}
+
 }  // extern "C"

@@ -1,6 +1,6 @@
 // Internal interface between the host ABI (capsule_host.cpp) and the HIP
-// kernels (capsule_copy.hip, linattn_scan.hip, kv_fp8.hip, append.hip).  Not part of the
-// public ABI.
+// kernels (capsule_copy.hip, linattn_scan.hip, gdn_scan.hip, kv_fp8.hip,
+// append.hip).  Not part of the public ABI.
 #pragma once
 
 #include <hip/hip_runtime_api.h>
@@ -66,6 +66,28 @@ struct ScanParams {
 };
 
 hipError_t launch_linattn_scan(const ScanParams& p, hipStream_t stream);
+
+// Gated delta-rule prefill (bf16 q/k/v, fp32 gates, write strengths and
+// state).  ws holds, per chunk of 64 tokens and head, the 64 x 64 fp32
+// inverse (I + A)^-1 of the chunk's delta-rule system, row-major
+// ([n_chunks][H][64][64]); the first launch writes it, the scan reads it.
+struct GdnParams {
+    const void*  q;
+    const void*  k;
+    const void*  v;
+    const float* g;
+    const float* beta;
+    const float* state_in;
+    float*       o;
+    float*       chunk_states;
+    float*       final_state;
+    float*       ws;
+    int64_t      T;
+    int32_t      H, dk, dv;
+    float        scale;
+};
+
+hipError_t launch_gdn(const GdnParams& p, hipStream_t stream);
 
 // FP8 (OCP E4M3) conversion of up to kFp8MaxSeg segments in one launch.
 // Segment s converts n_groups[s] groups of 16 elements from src[s] to

@@ -93,6 +93,17 @@ def linattn_inputs(seed: int, layer: int, T: int, H: int, dk: int, dv: int, dtyp
     return out
 
 
+def gdn_inputs(seed: int, layer: int, T: int, H: int, dk: int, dv: int, dtype: str = "bf16",
+               gate_mu: float = 3.0, gate_sigma: float = 0.5, t_offset_block: int = 0):
+    """linattn_inputs plus the write strengths 'beta' ([T,H] float32) of a
+    delta-rule layer: beta = sigmoid(x), x ~ N(0, 1), computed in fp64 and
+    rounded to fp32."""
+    out = linattn_inputs(seed, layer, T, H, dk, dv, dtype, gate_mu, gate_sigma, t_offset_block)
+    x = rng(seed, layer, "beta", t_offset_block).standard_normal(size=(T, H))
+    out["beta"] = (1.0 / (1.0 + np.exp(-x))).astype(np.float32)
+    return out
+
+
 def token_ids(seed: int, n: int, vocab: int = 151_936) -> np.ndarray:
     """Synthetic int32 token ids (metadata for the prefix digest only)."""
     return rng(seed, 0, "tokens").integers(0, vocab, size=n, dtype=np.int32)

@@ -158,6 +158,38 @@ def test_scan_argument_checks():
     assert _scan_status(T=0, q=0, k=0, v=0, g=0, o=0) == cap.CAP_OK
 
 
+def _gdn_status(**kw):
+    base = dict(q=4096, k=8192, v=12288, g=16384, beta=20480, state_in=0, o=1 << 30, chunk_states=0,
+                final_state=0, workspace=1 << 31, workspace_bytes=64 * 64 * 4, T=4, H=1, dk=64, dv=16, chunk=64,
+                in_dtype=cap.CAP_DTYPE_BF16, scale=1.0)
+    base.update(kw)
+    return N.load().gdn_chunked_prefill(ct.byref(N.gdn_args(**base)), None)
+
+
+def test_gdn_argument_checks():
+    L = N.load()
+    assert L.gdn_chunked_prefill(None, None) == cap.CAP_E_INVAL
+    assert L.gdn_workspace_bytes(0, 4, 64) == 0 and L.gdn_workspace_bytes(65, 3, 64) == 2 * 3 * 64 * 64 * 4
+    assert _gdn_status(T=-1) == cap.CAP_E_INVAL
+    assert _gdn_status(H=0) == cap.CAP_E_INVAL
+    assert _gdn_status(in_dtype=7) == cap.CAP_E_INVAL
+    assert _gdn_status(in_dtype=cap.CAP_DTYPE_F32) == cap.CAP_E_UNSUPPORTED
+    for name in ("q", "k", "v", "g", "beta", "o", "workspace"):
+        assert _gdn_status(**{name: 0}) == cap.CAP_E_INVAL, name
+    assert _gdn_status(chunk=32) == cap.CAP_E_UNSUPPORTED
+    assert _gdn_status(dk=96) == cap.CAP_E_UNSUPPORTED
+    assert _gdn_status(dv=24) == cap.CAP_E_UNSUPPORTED
+    assert _gdn_status(workspace_bytes=64 * 64 * 4 - 16) == cap.CAP_E_SIZE
+    assert _gdn_status(beta=20484) == cap.CAP_E_ALIGN
+    assert _gdn_status(workspace=(1 << 31) + 8) == cap.CAP_E_ALIGN
+    # the workspace overlapping an input, an output overlapping the workspace
+    assert _gdn_status(workspace=20480) == cap.CAP_E_INVAL
+    assert _gdn_status(o=(1 << 31) + 4096) == cap.CAP_E_INVAL
+    assert _gdn_status(o=12288 + 32) == cap.CAP_E_INVAL
+    # nothing to do: T = 0 without a final state returns at once, no workspace needed
+    assert _gdn_status(T=0, q=0, k=0, v=0, g=0, beta=0, o=0, workspace=0, workspace_bytes=0) == cap.CAP_OK
+
+
 def test_python_binding_has_no_fallback(tmp_path):
     with pytest.raises(ImportError):
         N.load(str(tmp_path / "missing.so"))

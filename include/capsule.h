@@ -298,8 +298,9 @@ CAP_API int linattn_chunked_prefill(const linattn_args* args, void* stream);
  *   beta : [T, H] fp32 write strengths (normally in [0, 1])
  *   state_in, chunk_states, final_state, o : as in linattn_args
  *   workspace : gdn_workspace_bytes(T, H, C) bytes of device scratch, 16-byte
- *               aligned; holds the per-chunk inverses (I + A)^-1 during the
- *               call (contents undefined afterwards).  May be NULL when T = 0.
+ *               aligned; holds the per-chunk inverses (I + A)^-1 and gate
+ *               tables during the call (contents undefined afterwards).  May
+ *               be NULL when T = 0.
  * Supported: chunk == 64, dk in {64, 128}, dv a multiple of 16, bf16 inputs.
  * Errors: CAP_E_INVAL (null required pointer, T < 0, H < 1, bad dtype,
  * overlapping buffers), CAP_E_SIZE (workspace_bytes too small),
@@ -325,8 +326,9 @@ typedef struct gdn_args {
     float        scale;
 } gdn_args;
 
-/* Workspace size for gdn_chunked_prefill: ceil(T / chunk) * H * chunk^2 * 4
- * bytes (0 for T <= 0, H < 1 or chunk < 1). */
+/* Workspace size for gdn_chunked_prefill: ceil(T / 64) * H * 12800 bytes
+ * (per chunk and head: the chunk's (I + A)^-1 in operand form and its gate
+ * tables); 0 for T <= 0, H < 1 or chunk != 64. */
 CAP_API uint64_t gdn_workspace_bytes(int64_t T, int32_t H, int32_t chunk);
 
 CAP_API int gdn_chunked_prefill(const gdn_args* args, void* stream);

@@ -625,9 +625,9 @@ int linattn_chunked_prefill(const linattn_args* a, void* stream) {
 }
 
 uint64_t gdn_workspace_bytes(int64_t T, int32_t H, int32_t chunk) {
-    if (T <= 0 || H < 1 || chunk < 1) return 0;
-    const uint64_t n = ((uint64_t)T + (uint64_t)chunk - 1) / (uint64_t)chunk;
-    return n * (uint64_t)H * (uint64_t)chunk * (uint64_t)chunk * 4u;
+    if (T <= 0 || H < 1 || chunk != 64) return 0;
+    const uint64_t n = ((uint64_t)T + 63) / 64;
+    return n * (uint64_t)H * (uint64_t)cap::kGdnWsRecord;
 }
 
 int gdn_chunked_prefill(const gdn_args* a, void* stream) {
@@ -674,7 +674,7 @@ int gdn_chunked_prefill(const gdn_args* a, void* stream) {
     cap::GdnParams p{};
     p.q = a->q; p.k = a->k; p.v = a->v; p.g = a->g; p.beta = a->beta;
     p.state_in = a->state_in; p.o = a->o; p.chunk_states = a->chunk_states; p.final_state = a->final_state;
-    p.ws = static_cast<float*>(a->workspace);
+    p.ws = static_cast<uint8_t*>(a->workspace);
     p.T = a->T; p.H = a->H; p.dk = a->dk; p.dv = a->dv;
     p.scale = a->scale;
     if (a->T == 0 && !a->final_state) return CAP_OK;

@@ -68,9 +68,14 @@ struct ScanParams {
 hipError_t launch_linattn_scan(const ScanParams& p, hipStream_t stream);
 
 // Gated delta-rule prefill (bf16 q/k/v, fp32 gates, write strengths and
-// state).  ws holds, per chunk of 64 tokens and head, the 64 x 64 fp32
-// inverse (I + A)^-1 of the chunk's delta-rule system, row-major
-// ([n_chunks][H][64][64]); the first launch writes it, the scan reads it.
+// state).  ws holds one record of kGdnWsRecord bytes per chunk of 64 tokens
+// and head ([n_chunks][H]), written by the first launch and read by the
+// scan: the causal blocks of the chunk's (I + A)^-1 as bf16 hi/lo MFMA
+// operands (6 blocks x 2 KiB, in the scan's lane order), then G log2(e)
+// (64 fp32, inclusive in-chunk log-gate sums) and beta (64 fp32).
+constexpr int64_t kGdnWsTBytes = 6 * 2048;
+constexpr int64_t kGdnWsRecord = kGdnWsTBytes + 2 * 64 * 4;
+
 struct GdnParams {
     const void*  q;
     const void*  k;
@@ -81,7 +86,7 @@ struct GdnParams {
     float*       o;
     float*       chunk_states;
     float*       final_state;
-    float*       ws;
+    uint8_t*     ws;
     int64_t      T;
     int32_t      H, dk, dv;
     float        scale;

@@ -16,28 +16,29 @@
 //
 // Two launches.
 //  1. gdn_prepare, one wave per (chunk, head), all chunks in parallel: A from
-//     K K^T on MFMA, then T = (I + A)^-1 by forward substitution in fp32
-//     (lane j owns column j), written to the workspace.  T depends on the
-//     chunk's keys, gates and write strengths only -- not on S -- and is the
-//     same for every value slice of the head, so it is computed once, off
-//     the sequential path.
+//     K K^T on MFMA, T = (I + A)^-1 by forward substitution in fp32 (lane j
+//     owns column j), and the decayed scores P = exp(G_i - G_m)(q_i . k_m),
+//     m <= i, on MFMA; both go to the workspace as ready MFMA operands.  T
+//     and P depend on the chunk's inputs only -- not on S -- and are the same
+//     for every value slice of the head, so they are computed once, off the
+//     sequential path.
 //  2. gdn_scan, one workgroup of eight waves per (head, 16-column slice of
 //     the values), walks the chunks in order.  Column slices are
 //     independent: U[:, J], o[:, J] and S[:, J] need only S[:, J] and
 //     v[:, J].  Only K S -> R -> U -> S is a true recurrence; it runs on
 //     four "chain" waves (row block r of the chunk, rows of S), with three
 //     LDS barriers per chunk:
-//       phase 1  R_r = beta (V_r - gamma K_r S) -> LDS
+//       phase 1  R_r = beta (V_r - gamma K_r S) -> LDS, and gamma Q_r S
+//                (the same S operands) for the output role
 //       phase 2  U_r = sum_m T[r rows][m] R_m -> LDS, with w_m U_m
 //       phase 3  S <- gamma_last S + K^T (w U) on the wave's rows of S,
-//                published as S^T for the next chunk.
-//     Four "output" waves do everything else beside it: X = Q_r S
-//     (phase 1), the decayed scores of their rows and the staging of the
-//     next chunk's K and gate tables (phase 2), o_r = scale (gamma X + P U)
-//     (phase 3), and the HBM loads three chunks ahead.  The arithmetic
-//     applied to a chunk depends only on (S, that chunk's inputs), so a
-//     call started at an aligned position from a restored state reproduces
-//     one longer call bit for bit.
+//                published for the next chunk.
+//     Four "output" waves do the rest beside it: the HBM loads (three
+//     chunks ahead) and the cooperative L2 prefetch (phase 1), staging the
+//     next chunk's K and gate tables (phase 2), and o_r = scale (gamma Q_r S
+//     + P U) (phase 3).  The arithmetic applied to a chunk depends only on
+//     (S, that chunk's inputs), so a call started at an aligned position from
+//     a restored state reproduces one longer call bit for bit.
 //
 // Every product runs on v_mfma_f32_16x16x32_bf16 with fp32 accumulation.
 // K and Q are exact bf16 operands; fp32 operands (S, R, U, w U, T, P) are
@@ -65,16 +66,22 @@ typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 __device__ inline float f32_of(uint32_t u) { return __builtin_bit_cast(float, u); }
 
 // ------------------------------------------------------------------ prepare
-// One wave per (chunk c, head h): T = (I + A)^-1 and the gate tables into
-// the workspace record of (c, h).  Rows past the last token have k = 0,
-// beta = 0 and g = 0, so their rows and columns of A vanish and T is the
-// identity there.
+// One wave per (chunk c, head h): T = (I + A)^-1, the decayed scores
+// P = exp(G_i - G_m) (q_i . k_m) (m <= i) and the gate tables into the
+// workspace record of (c, h).  Rows past the last token have q = k = 0,
+// beta = 0 and g = 0, so their rows and columns of A and P vanish and T is
+// the identity there.  T and P do not depend on the state and are the same
+// for every value slice of the head.
 //
-// Record layout (the scan's chain wave r reads block (r, i) for i <= r / 2):
-// block (r, i) = index r for r < 2, else 2 r - 2 + i; 2 KiB each, the bf16
-// hi plane then the lo plane, lane l = 16 grp + li holding
-// T[16 r + li][32 i + 8 grp .. +7] at byte 16 l of its plane.  After the six
-// blocks: G log2(e) (64 fp32) and beta (64 fp32).
+// Record layout (the scan's wave for row block r reads block (r, i) of T and
+// of P for i <= r / 2): block (r, i) = index r for r < 2, else 2 r - 2 + i;
+// 2 KiB each, the bf16 hi plane then the lo plane, lane l = 16 grp + li at
+// byte 16 l of its plane holding
+//   T: T[16 r + li][32 i + 8 grp + e],                 e = 0..7
+//   P: P[16 r + li][32 i + 16 (e / 4) + 4 grp + e % 4], e = 0..7
+// (P in the accumulator layout of K_s Q_r^T, which the scan uses as is as
+// the A operand of P U).  Six T blocks, six P blocks, then G log2(e)
+// (64 fp32) and beta (64 fp32).
 template <int DK>
 __global__ __launch_bounds__(64) void gdn_prepare_kernel(const GdnParams p) {
     constexpr int NKK = DK / 32;
@@ -98,6 +105,14 @@ __global__ __launch_bounds__(64) void gdn_prepare_kernel(const GdnParams p) {
         for (int kk = 0; kk < NKK; ++kk)
             kr[r][kk] = __builtin_amdgcn_raw_buffer_load_b128(
                 rk, (uint32_t)((16 * r + li) * krow + ((int64_t)h * DK + 32 * kk + 8 * grp) * 2), 0, 0);
+    const rsrc_t rq = make_rsrc(static_cast<const char*>(p.q) + t0 * krow, rows * krow);
+    u32x4 qr[4][NKK];  // same layout for the queries
+    #pragma unroll
+    for (int r = 0; r < 4; ++r)
+        #pragma unroll
+        for (int kk = 0; kk < NKK; ++kk)
+            qr[r][kk] = __builtin_amdgcn_raw_buffer_load_b128(
+                rq, (uint32_t)((16 * r + li) * krow + ((int64_t)h * DK + 32 * kk + 8 * grp) * 2), 0, 0);
     const rsrc_t rg = make_rsrc(p.g + t0 * H, rows * H * 4);
     const rsrc_t rb = make_rsrc(p.beta + t0 * H, rows * H * 4);
     const float gl = f32_of(__builtin_amdgcn_raw_buffer_load_b32(rg, (uint32_t)((lane * H + h) * 4), 0, 0));
@@ -126,6 +141,40 @@ __global__ __launch_bounds__(64) void gdn_prepare_kernel(const GdnParams p) {
             *reinterpret_cast<f32x4*>(&at[m * ATP + 16 * r + 4 * grp]) = a;
         }
     }
+
+    // P blocks: tile (r, s) = K_s Q_r^T holds P[16 r + li][16 s + 4 grp + q]
+    // in lane (grp, li), element q
+    uint8_t* rec = p.ws + (c * H + h) * kGdnWsRecord;
+    #pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const float gi = tg[16 * r + li];
+        #pragma unroll
+        for (int i = 0; i <= r / 2; ++i) {
+            float f[8];
+            #pragma unroll
+            for (int half = 0; half < 2; ++half) {
+                const int s = 2 * i + half;
+                if (s > r) {
+                    #pragma unroll
+                    for (int q = 0; q < 4; ++q) f[4 * half + q] = 0.0f;
+                    continue;
+                }
+                f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+                #pragma unroll
+                for (int kk = 0; kk < NKK; ++kk)
+                    acc = mma(__builtin_bit_cast(bf16x8, kr[s][kk]), __builtin_bit_cast(bf16x8, qr[r][kk]), acc);
+                const f32x4 gm = *reinterpret_cast<const f32x4*>(&tg[16 * s + 4 * grp]);
+                #pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    f[4 * half + q] = (s < r || 4 * grp + q <= li) ? acc[q] * exp2f(gi - gm[q]) : 0.0f;
+            }
+            bf16x8 hi, lo;
+            split_n<8>(f, hi, lo);
+            const int blk = r < 2 ? r : 2 * r - 2 + i;
+            *reinterpret_cast<bf16x8*>(rec + kGdnWsPOff + blk * 2048 + 16 * lane) = hi;
+            *reinterpret_cast<bf16x8*>(rec + kGdnWsPOff + blk * 2048 + 1024 + 16 * lane) = lo;
+        }
+    }
     __syncthreads();
 
     // column `lane` of T: x_t = [t == lane] - sum_{m<t} A_tm x_m, applied
@@ -150,7 +199,6 @@ __global__ __launch_bounds__(64) void gdn_prepare_kernel(const GdnParams p) {
     #pragma unroll
     for (int t = 0; t < CH; ++t) at[t * ATP + lane] = xv[t];
     __syncthreads();
-    uint8_t* rec = p.ws + (c * H + h) * kGdnWsRecord;
     #pragma unroll
     for (int r = 0; r < 4; ++r)
         #pragma unroll
@@ -165,7 +213,7 @@ __global__ __launch_bounds__(64) void gdn_prepare_kernel(const GdnParams p) {
             *reinterpret_cast<bf16x8*>(rec + blk * 2048 + 16 * lane) = hi;
             *reinterpret_cast<bf16x8*>(rec + blk * 2048 + 1024 + 16 * lane) = lo;
         }
-    float* tab = reinterpret_cast<float*>(rec + kGdnWsTBytes);
+    float* tab = reinterpret_cast<float*>(rec + kGdnWsTabOff);
     tab[lane] = tg[lane];
     tab[CH + lane] = tb[lane];
 }
@@ -180,15 +228,14 @@ struct alignas(16) GdnSmem {
     // 32 B at a time: a pitch of 16 B times an odd number whose 4-row windows
     // do not overlap keeps both conflict-free.
     static constexpr int KP = DK == 128 ? 152 : 104;
-    static constexpr int SP = DK + 8;     // S^T row pitch (elements)
-    static constexpr int RP = CH + 8;     // R^T / U^T row pitch (elements)
+    static constexpr int JP = DVS + 8;    // row pitch (elements) of the [*][j] tiles
     alignas(16) __bf16 k[2][CH * KP];     // K [m][d] by chunk parity
-    alignas(16) __bf16 q[2][CH * KP];     // Q [i][d] by chunk parity
-    alignas(16) __bf16 s[2][DVS * SP];    // S^T [j][d]: hi, lo
-    alignas(16) __bf16 r[2][DVS * RP];    // R^T [j][m]: hi, lo
-    alignas(16) __bf16 u[2][DVS * RP];    // U^T [j][m]: hi, lo
-    alignas(16) __bf16 wu[2][DVS * RP];   // (w U)^T [j][m], w_m = exp(G_last - G_m): hi, lo
+    alignas(16) __bf16 s[2][DK * JP];     // S [d][j]: hi, lo
+    alignas(16) __bf16 r[2][CH * JP];     // R [m][j]: hi, lo
+    alignas(16) __bf16 u[2][CH * JP];     // U [m][j]: hi, lo
+    alignas(16) __bf16 wu[2][CH * JP];    // w U [m][j], w_m = exp(G_last - G_m): hi, lo
     alignas(16) float tab[2][2 * CH];     // by chunk parity: G_m log2(e) (0..63), beta_m (64..127)
+    alignas(16) float x[NW][64 * 4];      // (gamma Q_r S)^T per row block, accumulator layout (lane order)
 };
 
 struct GdnCtx {
@@ -197,53 +244,67 @@ struct GdnCtx {
     int64_t qk_row, v_row, o_row;  // bytes per token of q / k, v, o
 };
 
-// Both roles walk the chunks four steps per loop iteration, so the register
-// stages (loads three chunks ahead) rotate without copies.  Every global
-// access of a step is issued unconditionally -- chunks past the end get
-// empty buffer ranges: loads read zeros, stores are dropped -- so the
-// in-order memory counters stay exact and loads issued after a step's stores
-// are waited for only three steps later.  A step past the end changes no
-// state, writes only LDS buffers no live step reads, and skips its barriers.
-// A call of at most one chunk (ONE) runs the step once, without prefetch.
+// Every product is computed transposed, with the value column j as the row
+// index of the accumulator: lane (grp, li) then holds four consecutive
+// columns j = 4 grp .. 4 grp + 3 of one token or one row of S, so v is read,
+// and o and the states are written, with one 8- or 16-byte access per lane
+// instead of one per element (the memory pipeline, not the arithmetic, is
+// what the scan waits on).  Tiles indexed [*][j] sit in LDS row-major and
+// are read as operands with the transposing LDS load.
+//
+// The output role walks the chunks four steps per loop iteration, so its
+// register stages (loads three chunks ahead) rotate without copies; the
+// chain role loads one chunk ahead, by which time the output role's L2
+// prefetch has the lines in L2.  Every global access of a step is issued
+// unconditionally -- chunks past the end get empty buffer ranges: loads read
+// zeros, stores are dropped -- so the in-order memory counters stay exact.
+// A step past the end changes no state, writes only LDS buffers no live
+// step reads, and skips its barriers.  A call of at most one chunk (ONE)
+// runs the step once, without prefetch.
 
 // ------------------------------------------------------------ output role
-// Wave R owns rows 16 R..16 R + 15 of the chunk: X = Q_R S (phase 1), the
-// decayed scores of its rows (phase 2), o = scale (gamma X + P U) (phase 3).
-// The role also loads K (all rows) and stages it in LDS, and wave 0 scans
-// the log-gates into the decay tables.
-template <int DK>
+// Wave R owns rows 16 R..16 R + 15 of the chunk: o^T = scale ((gamma X)^T +
+// U^T P^T) (phase 3) with (gamma X)^T from the chain role and P from the
+// workspace.  The role also loads K (all rows) and stages it in LDS, wave 0
+// stages the gate tables and waves 1 and 2 run the cooperative L2 prefetch.
+template <int DK, int R>
 struct OutStage {
-    static constexpr int PK = CH * DK / 8 / NO_T;  // 16-byte pieces of K and of Q per thread
-    u32x4 kp[PK];     // K pieces, coalesced (consecutive threads: consecutive bytes of a row)
-    u32x4 qp[PK];     // Q pieces, same order
-    float tab[2];     // wave 0: entries 2 lane, 2 lane + 1 of the gate tables
+    static constexpr int PK = CH * DK / 8 / NO_T;  // 16-byte K pieces per thread
+    static constexpr int NT2 = R / 2 + 1;
+    u32x4 kp[PK];       // K pieces, coalesced (consecutive threads: consecutive bytes of a row)
+    u32x4 p[NT2][2];    // P operand blocks (R, i): bf16 hi, lo
+    float tab[2];       // wave 0: entries 2 lane, 2 lane + 1 of the gate tables
 };
 
 template <int DK, bool ONE, int R>
 __device__ __forceinline__ void out_role(const GdnParams& p, GdnSmem<DK>& sm, const GdnCtx& x) {
     using Sm = GdnSmem<DK>;
-    using St = OutStage<DK>;
-    constexpr int KP = Sm::KP, SP = Sm::SP, RP = Sm::RP, NKK = DK / 32, PK = St::PK;
-    constexpr int NT2 = R / 2 + 1;  // 32-token steps of the causal rows of block R
+    using St = OutStage<DK, R>;
+    constexpr int KP = Sm::KP, JP = Sm::JP, PK = St::PK, NT2 = St::NT2;
     const int lane = x.lane, li = x.li, grp = x.grp, h = x.h, j0 = x.j0, H = x.H, dv = x.dv;
     const int ot = 64 * R + lane;
 
     auto load = [&](St& S_, int64_t c) {
         const int64_t t0 = c * CH, rows = x.T - t0;
         const rsrc_t rk = make_rsrc(static_cast<const char*>(p.k) + t0 * x.qk_row, rows * x.qk_row);
-        const rsrc_t rq = make_rsrc(static_cast<const char*>(p.q) + t0 * x.qk_row, rows * x.qk_row);
         #pragma unroll
         for (int u = 0; u < PK; ++u) {
             const int pc = ot + NO_T * u;
             const int m = pc / (DK / 8), d0 = (pc % (DK / 8)) * 8;
-            const uint32_t off = (uint32_t)(m * x.qk_row + ((int64_t)h * DK + d0) * 2);
-            S_.kp[u] = __builtin_amdgcn_raw_buffer_load_b128(rk, off, 0, 0);
-            S_.qp[u] = __builtin_amdgcn_raw_buffer_load_b128(rq, off, 0, 0);
+            S_.kp[u] = __builtin_amdgcn_raw_buffer_load_b128(rk, (uint32_t)(m * x.qk_row + ((int64_t)h * DK + d0) * 2), 0, 0);
+        }
+        const bool live = c < x.n;
+        const uint8_t* rec = p.ws + (live ? (c * H + h) * kGdnWsRecord : 0);
+        const rsrc_t rp = make_rsrc(rec + kGdnWsPOff, live ? kGdnWsTabOff - kGdnWsPOff : 0);
+        #pragma unroll
+        for (int i = 0; i < NT2; ++i) {
+            const int blk = R < 2 ? R : 2 * R - 2 + i;
+            #pragma unroll
+            for (int pl = 0; pl < 2; ++pl)
+                S_.p[i][pl] = __builtin_amdgcn_raw_buffer_load_b128(rp, (uint32_t)(blk * 2048 + pl * 1024 + 16 * lane), 0, 0);
         }
         if constexpr (R == 0) {
-            const bool live = c < x.n;
-            const rsrc_t rt = make_rsrc(p.ws + (live ? (c * H + h) * kGdnWsRecord + kGdnWsTBytes : 0),
-                                        live ? 2 * CH * 4 : 0);
+            const rsrc_t rt = make_rsrc(rec + kGdnWsTabOff, live ? 2 * CH * 4 : 0);
             const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(rt, (uint32_t)(8 * lane), 0, 0);
             const uint32_t v0 = v[0], v1 = v[1];
             S_.tab[0] = f32_of(v0);
@@ -251,14 +312,13 @@ __device__ __forceinline__ void out_role(const GdnParams& p, GdnSmem<DK>& sm, co
         }
     };
 
-    // K and Q rows into LDS buffer bk; wave 0 also the gate tables
+    // K rows into LDS buffer bk; wave 0 also the gate tables
     auto stage = [&](const St& S_, int bk) {
         #pragma unroll
         for (int u = 0; u < PK; ++u) {
             const int pc = ot + NO_T * u;
             const int m = pc / (DK / 8), d0 = (pc % (DK / 8)) * 8;
             *reinterpret_cast<u32x4*>(&sm.k[bk][m * KP + d0]) = S_.kp[u];
-            *reinterpret_cast<u32x4*>(&sm.q[bk][m * KP + d0]) = S_.qp[u];
         }
         if constexpr (R == 0) {
             sm.tab[bk][2 * lane] = S_.tab[0];
@@ -266,83 +326,75 @@ __device__ __forceinline__ void out_role(const GdnParams& p, GdnSmem<DK>& sm, co
         }
     };
 
-    auto step = [&](int64_t c, const St& nxt, St& ld) {
+    // Cooperative L2 prefetch.  The 16-column slices of a head all read the
+    // head's K, Q and workspace lines and share the lines of V; requested by
+    // every slice at the same moment, each miss costs every workgroup a full
+    // HBM latency.  So waves 1 and 2 of each slice touch the slice's share of
+    // the head's lines of chunk c + PREFETCH (the workspace record, then K,
+    // Q and V rows; line L goes to slice L % NS), two chunks ahead of the
+    // output role's loads, and the sibling slices' loads then hit in L2.  The
+    // fetched word is consumed only as an asm operand four steps later,
+    // which forces nothing but the load's completion.
+    constexpr int PREFETCH = 5;
+    uint32_t pf[4] = {0u, 0u, 0u, 0u};
+    auto prefetch = [&](int slot, int64_t c) {
+        __asm__ volatile("" : : "v"(pf[slot]));
+        const int64_t t0 = c * CH, rows = x.T - t0;
+        const int ns = dv / DVS;
+        const int L = j0 / DVS + ns * (64 * (R - 1) + lane);
+        constexpr int LK = DK * 2 / 128;            // 128-byte lines per row of K or Q
+        const int LV = (dv * 2 + 127) / 128;        // lines per row of the head's V
+        constexpr int nR = (int)((kGdnWsRecord + 127) / 128);
+        const int nK = CH * LK, nV = CH * LV;
+        const char* a = static_cast<const char*>(p.k);  // in bounds whenever the loop runs
+        if (L < nR) {
+            if (c < x.n) a = reinterpret_cast<const char*>(p.ws) + (c * H + h) * kGdnWsRecord + L * 128;
+        } else if (L < nR + 2 * nK) {
+            const int l = L - nR;
+            const int lq = l < nK ? l : l - nK, row = lq / LK;
+            if (row < rows)
+                a = static_cast<const char*>(l < nK ? p.k : p.q) + (t0 + row) * x.qk_row + h * DK * 2 + (lq % LK) * 128;
+        } else if (L < nR + 2 * nK + nV) {
+            const int l = L - nR - 2 * nK, row = l / LV;
+            if (row < rows) a = static_cast<const char*>(p.v) + (t0 + row) * x.v_row + h * dv * 2 + (l % LV) * 128;
+        }
+        pf[slot] = *reinterpret_cast<const uint32_t*>(a);
+    };
+
+    auto step = [&](int64_t c, const St& cur, const St& nxt, St& ld, int slot) {
         const bool live = c < x.n;
         const int b = (int)(c & 1);
         const int64_t t0 = c * CH, rows = x.T - t0;
         if constexpr (!ONE) load(ld, c + 3);
-
-        // ---- phase 1: X = Q_R S_c (S^T published by the chain role)
-        f32x4 xh = {0.f, 0.f, 0.f, 0.f}, xl = {0.f, 0.f, 0.f, 0.f};
-        bf16x8 qo[NKK];  // q[16 R + li][32 kk + 8 grp .. +7]
-        #pragma unroll
-        for (int kk = 0; kk < NKK; ++kk) {
-            qo[kk] = *reinterpret_cast<const bf16x8*>(&sm.q[b][(16 * R + li) * KP + 32 * kk + 8 * grp]);
-            const bf16x8 sh = *reinterpret_cast<const bf16x8*>(&sm.s[0][li * SP + 32 * kk + 8 * grp]);
-            const bf16x8 sl = *reinterpret_cast<const bf16x8*>(&sm.s[1][li * SP + 32 * kk + 8 * grp]);
-            xh = mma(qo[kk], sh, xh);
-            xl = mma(qo[kk], sl, xl);
-        }
+        if constexpr (!ONE && (R == 1 || R == 2)) prefetch(slot, c + PREFETCH);
+        // ---- phase 1: nothing but the loads above (the chain computes gamma X)
         if (live) lds_barrier();
 
-        // ---- phase 2: stage chunk c+1; P[i][m] = exp(G_i - G_m) (q_i . k_m),
-        // m <= i, i = 16 R + li, as the A operand of P U: element e of step i2
-        // is m = 32 i2 + 16 (e / 4) + 4 grp + e % 4 -- the accumulator layout
-        // of K_s Q_R^T, used as is
+        // ---- phase 2: stage chunk c+1
         if constexpr (!ONE) stage(nxt, b ^ 1);
-        const __bf16* kb = sm.k[b];
-        bf16x8 ph[NT2], pl[NT2];
-        const float g2i = sm.tab[b][16 * R + li];
-        #pragma unroll
-        for (int i2 = 0; i2 < NT2; ++i2) {
-            float pf[8];
-            #pragma unroll
-            for (int half = 0; half < 2; ++half) {
-                const int s = 2 * i2 + half;
-                if (s > R) {
-                    #pragma unroll
-                    for (int q = 0; q < 4; ++q) pf[4 * half + q] = 0.0f;
-                    continue;
-                }
-                f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-                #pragma unroll
-                for (int kk = 0; kk < NKK; ++kk) {
-                    const bf16x8 ko = *reinterpret_cast<const bf16x8*>(&kb[(16 * s + li) * KP + 32 * kk + 8 * grp]);
-                    acc = mma(ko, qo[kk], acc);
-                }
-                const f32x4 g2s = *reinterpret_cast<const f32x4*>(&sm.tab[b][16 * s + 4 * grp]);
-                #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const bool keep = s < R || 4 * grp + q <= li;
-                    pf[4 * half + q] = keep ? acc[q] * exp2f(g2i - g2s[q]) : 0.0f;
-                }
-            }
-            split_n<8>(pf, ph[i2], pl[i2]);
-        }
-        const f32x4 g2m = *reinterpret_cast<const f32x4*>(&sm.tab[b][16 * R + 4 * grp]);
-        f32x4 oa;
-        #pragma unroll
-        for (int q = 0; q < 4; ++q) oa[q] = exp2f(g2m[q]) * (xh[q] + xl[q]);
+        f32x4 oa = *reinterpret_cast<const f32x4*>(&sm.x[R][4 * lane]);
         if (live) lds_barrier();
 
-        // ---- phase 3: o_R = scale (gamma X + P U)
+        // ---- phase 3: o^T = scale ((gamma X)^T + U^T P^T); element e of the
+        // U^T operand of step i2 is m = 32 i2 + 16 (e / 4) + 4 grp + e % 4, the
+        // order of the P blocks
         #pragma unroll
         for (int i2 = 0; i2 < NT2; ++i2) {
-            const int m0 = li * RP + 32 * i2 + 4 * grp;
-            const bf16x8 uh = cat(*reinterpret_cast<const bf16x4*>(&sm.u[0][m0]),
-                                  *reinterpret_cast<const bf16x4*>(&sm.u[0][m0 + 16]));
-            const bf16x8 ul = cat(*reinterpret_cast<const bf16x4*>(&sm.u[1][m0]),
-                                  *reinterpret_cast<const bf16x4*>(&sm.u[1][m0 + 16]));
-            oa = mma(ph[i2], uh, oa);
-            oa = mma(ph[i2], ul, oa);
-            oa = mma(pl[i2], uh, oa);
+            const bf16x8 ph = __builtin_bit_cast(bf16x8, cur.p[i2][0]);
+            const bf16x8 pl = __builtin_bit_cast(bf16x8, cur.p[i2][1]);
+            const int m0 = 32 * i2 + 4 * grp;
+            const bf16x8 uh = cat(tr4(sm.u[0], JP, m0, 0, li), tr4(sm.u[0], JP, m0 + 16, 0, li));
+            const bf16x8 ul = cat(tr4(sm.u[1], JP, m0, 0, li), tr4(sm.u[1], JP, m0 + 16, 0, li));
+            oa = mma(uh, ph, oa);
+            oa = mma(ul, ph, oa);
+            oa = mma(uh, pl, oa);
         }
         const rsrc_t ro = make_rsrc(static_cast<char*>(static_cast<void*>(p.o)) + t0 * x.o_row, rows * x.o_row);
+        f32x4 os;
         #pragma unroll
-        for (int q = 0; q < 4; ++q)
-            __builtin_amdgcn_raw_buffer_store_b32(
-                __builtin_bit_cast(uint32_t, oa[q] * p.scale), ro,
-                (uint32_t)((16 * R + 4 * grp + q) * x.o_row + ((int64_t)h * dv + j0 + li) * 4), 0, 0);
+        for (int q = 0; q < 4; ++q) os[q] = oa[q] * p.scale;
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, os), ro,
+                                               (uint32_t)((16 * R + li) * x.o_row + ((int64_t)h * dv + j0 + 4 * grp) * 4), 0, 0);
         if (live) lds_barrier();
     };
 
@@ -351,7 +403,7 @@ __device__ __forceinline__ void out_role(const GdnParams& p, GdnSmem<DK>& sm, co
         load(s0, 0);
         stage(s0, 0);
         lds_barrier();
-        if (x.n == 1) step(0, s0, s0);
+        if (x.n == 1) step(0, s0, s0, s0, 0);
     } else {
         St s0, s1, s2, s3;
         load(s0, 0);
@@ -360,58 +412,56 @@ __device__ __forceinline__ void out_role(const GdnParams& p, GdnSmem<DK>& sm, co
         stage(s0, 0);
         lds_barrier();
         for (int64_t c = 0; c < x.n; c += 4) {
-            step(c, s1, s3);
-            step(c + 1, s2, s0);
-            step(c + 2, s3, s1);
-            step(c + 3, s0, s2);
+            step(c, s0, s1, s3, 0);
+            step(c + 1, s1, s2, s0, 1);
+            step(c + 2, s2, s3, s1, 2);
+            step(c + 3, s3, s0, s2, 3);
         }
     }
 }
 
 // ------------------------------------------------------------- chain role
 // Wave R owns rows 16 R..16 R + 15 of the chunk and rows
-// 16 R NDW..16 (R + 1) NDW - 1 of S (fp32, in registers): K_R S -> R
-// (phase 1), U_R = T[R rows] R (phase 2), S <- gamma_last S + K^T (w U) on
-// its rows of S and S^T published (phase 3).  Only this role's work is on
-// the state's sequential path.
-template <int R>
+// 16 R NDW..16 (R + 1) NDW - 1 of S (fp32, in registers): (K_R S)^T -> R
+// (phase 1), U_R^T = R^T T[R rows]^T (phase 2), S^T <- gamma_last S^T +
+// (w U)^T K on its rows of S, published for the next chunk (phase 3).  Only
+// this role's work is on the state's sequential path.
+template <int DK, int R>
 struct ChainStage {
     static constexpr int NT2 = R / 2 + 1;
     u32x4 t[NT2][2];    // T[16 R + li][32 i + 8 grp .. +7]: bf16 hi, lo
-    uint32_t v[4];      // bf16 bits of v[16 R + 4 grp + q][j0 + li]
+    u32x4 q[DK / 32];   // q[16 R + li][32 kk + 8 grp .. +7]
+    u32x2 v;            // bf16 v[16 R + li][j0 + 4 grp .. +3]
 };
 
 template <int DK, bool ONE, int R>
 __device__ __forceinline__ void chain_role(const GdnParams& p, GdnSmem<DK>& sm, const GdnCtx& x) {
     using Sm = GdnSmem<DK>;
-    using St = ChainStage<R>;
-    constexpr int KP = Sm::KP, SP = Sm::SP, RP = Sm::RP;
+    using St = ChainStage<DK, R>;
+    constexpr int KP = Sm::KP, JP = Sm::JP;
     constexpr int NKK = DK / 32, NDW = DK / 64, NT2 = St::NT2;
     const int li = x.li, grp = x.grp, h = x.h, j0 = x.j0, H = x.H, dv = x.dv;
 
-    // state tiles in accumulator layout: S[u][q] = S[d][j0 + li] with
-    // d = 16 (R NDW + u) + 4 grp + q; for each q the 16 lanes of a group hold
-    // 64 contiguous bytes of a state row
+    // state tiles in transposed accumulator layout: S[u][q] = S[d][j0 + 4 grp
+    // + q] with d = 16 (R NDW + u) + li -- 16 contiguous bytes of a state row
     f32x4 S[NDW];
-    auto srow = [&](int u, int q) -> int64_t {
-        return ((int64_t)h * DK + 16 * (R * NDW + u) + 4 * grp + q) * dv + j0 + li;
+    auto srow = [&](int u) -> int64_t {  // element offset of S[d][j0 + 4 grp] in a [H][dk][dv] state
+        return ((int64_t)h * DK + 16 * (R * NDW + u) + li) * dv + j0 + 4 * grp;
     };
     #pragma unroll
-    for (int u = 0; u < NDW; ++u) {
-        S[u] = f32x4{0.f, 0.f, 0.f, 0.f};
-        if (p.state_in) {
-            #pragma unroll
-            for (int q = 0; q < 4; ++q) S[u][q] = p.state_in[srow(u, q)];
-        }
-    }
+    for (int u = 0; u < NDW; ++u)
+        S[u] = p.state_in ? *reinterpret_cast<const f32x4*>(p.state_in + srow(u)) : f32x4{0.f, 0.f, 0.f, 0.f};
 
     auto load = [&](St& S_, int64_t c) {
         const int64_t t0 = c * CH, rows = x.T - t0;
         const rsrc_t rv = make_rsrc(static_cast<const char*>(p.v) + t0 * x.v_row, rows * x.v_row);
+        S_.v = __builtin_amdgcn_raw_buffer_load_b64(
+            rv, (uint32_t)((16 * R + li) * x.v_row + ((int64_t)h * dv + j0 + 4 * grp) * 2), 0, 0);
+        const rsrc_t rq = make_rsrc(static_cast<const char*>(p.q) + t0 * x.qk_row, rows * x.qk_row);
         #pragma unroll
-        for (int q = 0; q < 4; ++q)
-            S_.v[q] = __builtin_amdgcn_raw_buffer_load_b16(
-                rv, (uint32_t)((16 * R + 4 * grp + q) * x.v_row + ((int64_t)h * dv + j0 + li) * 2), 0, 0);
+        for (int kk = 0; kk < NKK; ++kk)
+            S_.q[kk] = __builtin_amdgcn_raw_buffer_load_b128(
+                rq, (uint32_t)((16 * R + li) * x.qk_row + ((int64_t)h * DK + 32 * kk + 8 * grp) * 2), 0, 0);
         const bool live = c < x.n;
         const rsrc_t rt = make_rsrc(p.ws + (live ? (c * H + h) * kGdnWsRecord : 0), live ? kGdnWsTBytes : 0);
         #pragma unroll
@@ -423,71 +473,78 @@ __device__ __forceinline__ void chain_role(const GdnParams& p, GdnSmem<DK>& sm, 
         }
     };
 
-    // this wave's rows of S as bf16 hi/lo planes of S^T [j][d]
+    // this wave's rows of S as bf16 hi/lo planes of S [d][j]
     auto publish_s = [&]() {
         #pragma unroll
         for (int u = 0; u < NDW; ++u) {
-            const int d0 = 16 * (R * NDW + u) + 4 * grp;
+            const int d = 16 * (R * NDW + u) + li;
             const float f[4] = {S[u][0], S[u][1], S[u][2], S[u][3]};
             bf16x4 hi, lo;
             split_n<4>(f, hi, lo);
-            *reinterpret_cast<bf16x4*>(&sm.s[0][li * SP + d0]) = hi;
-            *reinterpret_cast<bf16x4*>(&sm.s[1][li * SP + d0]) = lo;
+            *reinterpret_cast<bf16x4*>(&sm.s[0][d * JP + 4 * grp]) = hi;
+            *reinterpret_cast<bf16x4*>(&sm.s[1][d * JP + 4 * grp]) = lo;
         }
     };
 
-    const uint64_t state_bytes = (uint64_t)H * DK * dv * 4;
     // the chain waves carry the sequential path: issue their instructions
     // first when they compete with the output wave on the same SIMD
     __builtin_amdgcn_s_setprio(2);
+    const int64_t state_elems = (int64_t)H * DK * dv;
     auto step = [&](int64_t c, const St& cur, St& ld) {
         const bool live = c < x.n;
         const int b = (int)(c & 1);
         const __bf16* kb = sm.k[b];
-        if constexpr (!ONE) load(ld, c + 3);
 
-        // operands and decays that do not depend on S
+        // operands and decays that do not depend on S (token m = 16 R + li)
         bf16x8 th[NT2], tl[NT2];
         #pragma unroll
         for (int i2 = 0; i2 < NT2; ++i2) {
             th[i2] = __builtin_bit_cast(bf16x8, cur.t[i2][0]);
             tl[i2] = __builtin_bit_cast(bf16x8, cur.t[i2][1]);
         }
-        const f32x4 g2m = *reinterpret_cast<const f32x4*>(&sm.tab[b][16 * R + 4 * grp]);
-        const f32x4 bm = *reinterpret_cast<const f32x4*>(&sm.tab[b][CH + 16 * R + 4 * grp]);
+        const float g2 = sm.tab[b][16 * R + li], bt = sm.tab[b][CH + 16 * R + li];
         const float g2l = sm.tab[b][CH - 1];
-        float gam[4], wm[4], vv[4];
-        #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            gam[q] = exp2f(g2m[q]);
-            wm[q] = exp2f(g2l - g2m[q]);
-            vv[q] = f32_of(cur.v[q] << 16);
-        }
-        const float gl = exp2f(g2l);
+        const float gam = exp2f(g2), wm = exp2f(g2l - g2), gl = exp2f(g2l);
+        const uint32_t v0 = cur.v[0], v1 = cur.v[1];
+        const float vv[4] = {f32_of(v0 << 16), f32_of(v0 & 0xFFFF0000u), f32_of(v1 << 16), f32_of(v1 & 0xFFFF0000u)};
 
-        // ---- phase 1: R_R = beta (V_R - gamma K_R S_c)
+        // ---- phase 1: R^T = beta (V - gamma K_R S_c)^T, and (gamma Q_R S_c)^T for
+        // the output role (element e of the S^T operand of step kk is
+        // d = 32 kk + 8 grp + e)
         f32x4 kh = {0.f, 0.f, 0.f, 0.f}, kl = {0.f, 0.f, 0.f, 0.f};
+        f32x4 xh = {0.f, 0.f, 0.f, 0.f}, xl = {0.f, 0.f, 0.f, 0.f};
         #pragma unroll
         for (int kk = 0; kk < NKK; ++kk) {
-            const bf16x8 ko = *reinterpret_cast<const bf16x8*>(&kb[(16 * R + li) * KP + 32 * kk + 8 * grp]);
-            const bf16x8 sh = *reinterpret_cast<const bf16x8*>(&sm.s[0][li * SP + 32 * kk + 8 * grp]);
-            const bf16x8 sl = *reinterpret_cast<const bf16x8*>(&sm.s[1][li * SP + 32 * kk + 8 * grp]);
-            kh = mma(ko, sh, kh);
-            kl = mma(ko, sl, kl);
+            const int d0 = 32 * kk + 8 * grp;
+            const bf16x8 sh = cat(tr4(sm.s[0], JP, d0, 0, li), tr4(sm.s[0], JP, d0 + 4, 0, li));
+            const bf16x8 sl = cat(tr4(sm.s[1], JP, d0, 0, li), tr4(sm.s[1], JP, d0 + 4, 0, li));
+            const bf16x8 ko = *reinterpret_cast<const bf16x8*>(&kb[(16 * R + li) * KP + d0]);
+            const bf16x8 qo = __builtin_bit_cast(bf16x8, cur.q[kk]);
+            kh = mma(sh, ko, kh);
+            kl = mma(sl, ko, kl);
+            xh = mma(sh, qo, xh);
+            xl = mma(sl, qo, xl);
         }
+        // the next chunk's loads go after this phase's LDS reads, so a full
+        // memory pipeline cannot hold those reads back
+        if constexpr (!ONE) load(ld, c + 1);
         {
+            f32x4 xg;
+            #pragma unroll
+            for (int q = 0; q < 4; ++q) xg[q] = gam * (xh[q] + xl[q]);
+            *reinterpret_cast<f32x4*>(&sm.x[R][4 * x.lane]) = xg;
             float rr[4];
             #pragma unroll
-            for (int q = 0; q < 4; ++q) rr[q] = bm[q] * (vv[q] - gam[q] * (kh[q] + kl[q]));
+            for (int q = 0; q < 4; ++q) rr[q] = bt * (vv[q] - gam * (kh[q] + kl[q]));
             bf16x4 hi, lo;
             split_n<4>(rr, hi, lo);
-            *reinterpret_cast<bf16x4*>(&sm.r[0][li * RP + 16 * R + 4 * grp]) = hi;
-            *reinterpret_cast<bf16x4*>(&sm.r[1][li * RP + 16 * R + 4 * grp]) = lo;
+            *reinterpret_cast<bf16x4*>(&sm.r[0][(16 * R + li) * JP + 4 * grp]) = hi;
+            *reinterpret_cast<bf16x4*>(&sm.r[1][(16 * R + li) * JP + 4 * grp]) = lo;
         }
         if (live) lds_barrier();
 
-        // ---- phase 2: U_R = T[R rows] R, and w U
-        bf16x8 kt[NDW][2];  // K^T operands of the update (element e: m = 32 mm + 8 grp + e)
+        // ---- phase 2: U_R^T = R^T T[R rows]^T, and (w U_R)^T
+        bf16x8 kt[NDW][2];  // K operands of the update (element e: m = 32 mm + 8 grp + e)
         #pragma unroll
         for (int u = 0; u < NDW; ++u)
             #pragma unroll
@@ -498,40 +555,36 @@ __device__ __forceinline__ void chain_role(const GdnParams& p, GdnSmem<DK>& sm, 
         f32x4 ua = {0.f, 0.f, 0.f, 0.f}, ub = {0.f, 0.f, 0.f, 0.f}, uc = {0.f, 0.f, 0.f, 0.f};
         #pragma unroll
         for (int i2 = 0; i2 < NT2; ++i2) {
-            const bf16x8 rh = *reinterpret_cast<const bf16x8*>(&sm.r[0][li * RP + 32 * i2 + 8 * grp]);
-            const bf16x8 rl = *reinterpret_cast<const bf16x8*>(&sm.r[1][li * RP + 32 * i2 + 8 * grp]);
-            ua = mma(th[i2], rh, ua);
-            ub = mma(th[i2], rl, ub);
-            uc = mma(tl[i2], rh, uc);
+            const int m0 = 32 * i2 + 8 * grp;
+            const bf16x8 rh = cat(tr4(sm.r[0], JP, m0, 0, li), tr4(sm.r[0], JP, m0 + 4, 0, li));
+            const bf16x8 rl = cat(tr4(sm.r[1], JP, m0, 0, li), tr4(sm.r[1], JP, m0 + 4, 0, li));
+            ua = mma(rh, th[i2], ua);
+            ub = mma(rl, th[i2], ub);
+            uc = mma(rh, tl[i2], uc);
         }
         {
             float uf[4], wf[4];
             #pragma unroll
             for (int q = 0; q < 4; ++q) {
                 uf[q] = ua[q] + (ub[q] + uc[q]);
-                wf[q] = uf[q] * wm[q];
+                wf[q] = uf[q] * wm;
             }
             bf16x4 hi, lo;
             split_n<4>(uf, hi, lo);
-            *reinterpret_cast<bf16x4*>(&sm.u[0][li * RP + 16 * R + 4 * grp]) = hi;
-            *reinterpret_cast<bf16x4*>(&sm.u[1][li * RP + 16 * R + 4 * grp]) = lo;
+            *reinterpret_cast<bf16x4*>(&sm.u[0][(16 * R + li) * JP + 4 * grp]) = hi;
+            *reinterpret_cast<bf16x4*>(&sm.u[1][(16 * R + li) * JP + 4 * grp]) = lo;
             split_n<4>(wf, hi, lo);
-            *reinterpret_cast<bf16x4*>(&sm.wu[0][li * RP + 16 * R + 4 * grp]) = hi;
-            *reinterpret_cast<bf16x4*>(&sm.wu[1][li * RP + 16 * R + 4 * grp]) = lo;
+            *reinterpret_cast<bf16x4*>(&sm.wu[0][(16 * R + li) * JP + 4 * grp]) = hi;
+            *reinterpret_cast<bf16x4*>(&sm.wu[1][(16 * R + li) * JP + 4 * grp]) = lo;
         }
         if (live) lds_barrier();
 
-        // ---- phase 3: S_c to chunk_states[c]; S <- gamma_last S + K^T (w U)
-        const rsrc_t rc = make_rsrc(p.chunk_states + (live ? c : 0) * (int64_t)H * DK * dv,
-                                    live && p.chunk_states ? (int64_t)state_bytes : 0);
+        // ---- phase 3: S_c to chunk_states[c]; S^T <- gamma_last S^T + (w U)^T K
+        const rsrc_t rc = make_rsrc(p.chunk_states + (live ? c : 0) * state_elems,
+                                    live && p.chunk_states ? state_elems * 4 : 0);
         #pragma unroll
         for (int u = 0; u < NDW; ++u)
-            #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const float sv = S[u][q];  // a bit_cast of a vector element reads element 0
-                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, sv), rc,
-                                                      (uint32_t)(srow(u, q) * 4), 0, 0);
-            }
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, S[u]), rc, (uint32_t)(srow(u) * 4), 0, 0);
         #pragma unroll
         for (int u = 0; u < NDW; ++u) {
             f32x4 ah, al = {0.f, 0.f, 0.f, 0.f};
@@ -539,11 +592,11 @@ __device__ __forceinline__ void chain_role(const GdnParams& p, GdnSmem<DK>& sm, 
             for (int q = 0; q < 4; ++q) ah[q] = gl * S[u][q];
             #pragma unroll
             for (int mm = 0; mm < 2; ++mm) {
-                const int m0 = li * RP + 32 * mm + 8 * grp;
-                const bf16x8 wh = *reinterpret_cast<const bf16x8*>(&sm.wu[0][m0]);
-                const bf16x8 wl = *reinterpret_cast<const bf16x8*>(&sm.wu[1][m0]);
-                ah = mma(kt[u][mm], wh, ah);
-                al = mma(kt[u][mm], wl, al);
+                const int m0 = 32 * mm + 8 * grp;
+                const bf16x8 wh = cat(tr4(sm.wu[0], JP, m0, 0, li), tr4(sm.wu[0], JP, m0 + 4, 0, li));
+                const bf16x8 wl = cat(tr4(sm.wu[1], JP, m0, 0, li), tr4(sm.wu[1], JP, m0 + 4, 0, li));
+                ah = mma(wh, kt[u][mm], ah);
+                al = mma(wl, kt[u][mm], al);
             }
             if (live) S[u] = ah + al;
         }
@@ -558,24 +611,20 @@ __device__ __forceinline__ void chain_role(const GdnParams& p, GdnSmem<DK>& sm, 
         lds_barrier();
         if (x.n == 1) step(0, s0, s0);
     } else {
-        St s0, s1, s2, s3;
+        // one chunk ahead is enough here: the output role's prefetch has the
+        // lines in L2 by then
+        St s0, s1;
         load(s0, 0);
-        load(s1, 1);
-        load(s2, 2);
         publish_s();
         lds_barrier();
-        for (int64_t c = 0; c < x.n; c += 4) {
-            step(c, s0, s3);
+        for (int64_t c = 0; c < x.n; c += 2) {
+            step(c, s0, s1);
             step(c + 1, s1, s0);
-            step(c + 2, s2, s1);
-            step(c + 3, s3, s2);
         }
     }
     if (p.final_state) {
         #pragma unroll
-        for (int u = 0; u < NDW; ++u)
-            #pragma unroll
-            for (int q = 0; q < 4; ++q) p.final_state[srow(u, q)] = S[u][q];
+        for (int u = 0; u < NDW; ++u) *reinterpret_cast<f32x4*>(p.final_state + srow(u)) = S[u];
     }
 }
 

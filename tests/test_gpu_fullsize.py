@@ -1,5 +1,6 @@
 """Full-size cases in the launch configuration bench.py times: one 48-layer
-workload layer (16384 tokens x 32 heads, dk = dv = 128) against the oracle on
+workload layer (16384 tokens x 32 heads, dk = dv = 128) of the
+linear-attention scan and of the gated delta-rule scan against the oracle on
 sampled heads, the full 881,983,488-byte capsule against the oracle's memcpy,
 fork x4, and the robot-reset workload (32 environments, gallery of 8
 capsules, 1000 batched gather-restores)."""
@@ -36,6 +37,36 @@ def test_hybrid48_layer_sampled_heads(orc):
     e_s = rel_err(fs[heads].cpu().numpy(), s_ref)
     e_c = max(rel_err(cs[j][heads].cpu().numpy(), cs_ref[j]) for j in (1, 100, 128, 255))
     print("16k x 32 heads, heads %s: rel err o %.3g final %.3g chunk states %.3g" % (heads, e_o, e_s, e_c))
+    assert e_o <= PARITY_TOL and e_s <= PARITY_TOL and e_c <= PARITY_TOL
+    assert e_o <= SPLIT_TOL and e_s <= SPLIT_TOL and e_c <= SPLIT_TOL
+    assert torch.isfinite(o).all() and torch.isfinite(cs).all()
+
+
+def test_hybrid48_gdn_layer_sampled_heads(orc):
+    """The delta-rule prefill at the same layer shape, one call over all 16384
+    tokens; o, chunk states and the final state of three heads against the
+    oracle (sequential recurrence for o and the final state, chunked form for
+    the chunk states)."""
+    w = H48
+    T, H, dk, dv = w.prefix, w.heads, w.dk, w.dv
+    inp = synth.gdn_inputs(w.seed, 0, T, H, dk, dv, "bf16")
+    d = dev_inputs(inp)
+    beta = torch.from_numpy(inp["beta"]).cuda()
+    n_chunks = T // 64
+    o = torch.empty((T, H, dv), dtype=torch.float32, device="cuda")
+    cs = torch.empty((n_chunks, H, dk, dv), dtype=torch.float32, device="cuda")
+    fs = torch.empty((H, dk, dv), dtype=torch.float32, device="cuda")
+    cap.gdn_chunked_prefill(d["q"], d["k"], d["v"], d["g"], beta, o, chunk_states=cs, final_state=fs)
+    torch.cuda.synchronize()
+    heads = [0, 17, 31]
+    sub = {n: np.ascontiguousarray(inp[n][:, heads]) for n in ("q", "k", "v", "g", "beta")}
+    a = (sub["q"], sub["k"], sub["v"], sub["g"], sub["beta"])
+    o_ref, s_ref = orc.gdn_sequential(*a)
+    _, cs_ref, _ = orc.gdn_chunked(*a, 64)
+    e_o = rel_err(o[:, heads].cpu().numpy(), o_ref)
+    e_s = rel_err(fs[heads].cpu().numpy(), s_ref)
+    e_c = max(rel_err(cs[j][heads].cpu().numpy(), cs_ref[j]) for j in (1, 100, 128, 255))
+    print("gdn 16k x 32 heads, heads %s: rel err o %.3g final %.3g chunk states %.3g" % (heads, e_o, e_s, e_c))
     assert e_o <= PARITY_TOL and e_s <= PARITY_TOL and e_c <= PARITY_TOL
     assert e_o <= SPLIT_TOL and e_s <= SPLIT_TOL and e_c <= SPLIT_TOL
     assert torch.isfinite(o).all() and torch.isfinite(cs).all()

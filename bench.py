@@ -17,6 +17,10 @@ linear layer.  One step is one pass of the whole hot path:
 Every phase is bracketed by HIP events recorded on the stream the kernels run
 on.  restore/cold TTFT = (phase 2 + phase 6) / (phase 4 + phase 6).
 
+After the timed steps, one gated delta-rule layer of the same shape (the
+model family's Gated DeltaNet state; q/k/v bf16, gates and write strengths
+fp32) is timed on its own under `gdn`.
+
 The JSON line's `value` is the capsule restore bandwidth (GB/s, bytes read +
 written); the scan and TTFT figures ride along as extra keys.  `roofline`
 covers the dominant kernel (the scan, phase 1) and `roofline_copy` the restore.
@@ -78,6 +82,13 @@ def scan_bytes(T, H, dk, dv, chunk_states):
     return b
 
 
+def gdn_bytes(T, H, dk, dv):
+    """Algorithmic HBM bytes of one delta-rule prefill call with chunk states
+    (bf16 q,k,v; fp32 g, beta, o, states; zero entering state)."""
+    n_chunks = (T + 63) // 64
+    return T * H * (2 * (2 * dk + dv) + 8 + 4 * dv) + (n_chunks + 1) * H * dk * dv * 4
+
+
 def scan_useful_flops(T, H, dk, dv, C=64):
     """Causal useful flops: per chunk of L tokens, QK^T over the causal half,
     P V, Q S and the state fold."""
@@ -128,6 +139,11 @@ def cpu_baseline(w, capsule_layout):
     orc.sequential(inp["q"], inp["k"], inp["v"], inp["g"])
     t_scan = time.perf_counter() - t0
     stack_tok_s = w.prefix / (t_scan * w.n_linear * (w.heads / H_s))
+    # delta rule: the token-by-token recurrence on 1 layer x 2 heads
+    ginp = synth.gdn_inputs(w.seed, 0, w.prefix, H_s, w.dk, w.dv, "bf16")
+    t0 = time.perf_counter()
+    orc.gdn_sequential(ginp["q"], ginp["k"], ginp["v"], ginp["g"], ginp["beta"])
+    t_gdn = time.perf_counter() - t0
     return {
         "cpu_baseline": {
             "value": round(restore_gbs, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
@@ -139,6 +155,13 @@ def cpu_baseline(w, capsule_layout):
             "sample": "oracle sequential recurrence (fp64, single thread) on 1 layer x %d of %d heads x %d tokens "
                       "in %.2f s, extrapolated x%d layers x%d head groups" % (
                           H_s, w.heads, w.prefix, t_scan, w.n_linear, w.heads // H_s),
+        },
+        "cpu_baseline_gdn": {
+            "value": round(w.prefix / (t_gdn * (w.heads / H_s)), 3), "unit": "tokens/s per layer", "cores": 1,
+            "kind": "oracle",
+            "sample": "oracle gated delta-rule recurrence (fp64, single thread) on 1 layer x %d of %d heads x %d "
+                      "tokens in %.2f s, extrapolated x%d head groups" % (
+                          H_s, w.heads, w.prefix, t_gdn, w.heads // H_s),
         },
     }
 
@@ -412,6 +435,35 @@ def main():
     stream.synchronize()
     assert torch.equal(chk, kv[0][1][: 2 * P * kv_el].view(torch.bfloat16))
 
+    # gated delta-rule layer (same shape as a linear-attention layer of the
+    # stack): one call = the (I + A)^-1 / score launch + the scan launch
+    ginp = synth.gdn_inputs(w.seed, 0, T, H, dk, dv, "bf16")
+    gd = {n: torch.from_numpy(ginp[n + "_dev"].view(np.int16)).view(torch.bfloat16).to(dev) for n in ("q", "k", "v")}
+    gd["g"] = torch.from_numpy(ginp["g"]).to(dev)
+    gd["beta"] = torch.from_numpy(ginp["beta"]).to(dev)
+    del ginp
+    g_o = torch.empty((T, H, dv), dtype=torch.float32, device=dev)
+    g_cs = torch.empty(((T + 63) // 64, H, dk, dv), dtype=torch.float32, device=dev)
+    g_fs = torch.empty((H, dk, dv), dtype=torch.float32, device=dev)
+    g_ws = torch.empty(cap.gdn_workspace_bytes(T, H), dtype=torch.uint8, device=dev)
+    g_ms = []
+    with torch.cuda.stream(stream):
+        for rnd in range(5):
+            flush.fill_(rnd)
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            e[0].record(stream)
+            cap.gdn_chunked_prefill(gd["q"], gd["k"], gd["v"], gd["g"], gd["beta"], g_o, chunk_states=g_cs,
+                                    final_state=g_fs, workspace=g_ws, stream=stream)
+            e[1].record(stream)
+            stream.synchronize()
+            if rnd:
+                g_ms.append(e[0].elapsed_time(e[1]))
+    gdn_ms = float(np.median(g_ms))
+    gdn_b = gdn_bytes(T, H, dk, dv)
+    gdn_gbs = gdn_b / (gdn_ms * 1e-3) / 1e9
+    assert bool(torch.isfinite(g_o).all()) and bool(torch.isfinite(g_fs).all())
+    del gd, g_o, g_cs, g_fs
+
     scan_b = scan_bytes(T, H, dk, dv, True)
     scan_b_final = scan_bytes(T, H, dk, dv, False)
     flops = scan_useful_flops(T, H, dk, dv)
@@ -478,6 +530,13 @@ def main():
                    "quantize_gbs": round(conv_bytes / (f8ms["quantize"] * 1e-3) / 1e9, 2),
                    "capsule_ttft_ms": round(f8ms["restore"] + f8ms["rebuild"] + ms["continue"], 4),
                    "capsule_ttft_ms_lazy_none": round(f8ms["restore"] + ms["continue"], 4)},
+        "gdn": {"what": "gated delta-rule prefill, one layer (H=%d, dk=dv=%d, %d tokens, chunk states): "
+                        "(I + A)^-1 and scores launch + scan launch" % (H, dk, T),
+                "layer_ms": round(gdn_ms, 4), "tokens_per_s": round(T / (gdn_ms * 1e-3), 1),
+                "stack_tokens_per_s_36_layers": round(T / (n_lin * gdn_ms * 1e-3), 1),
+                "roofline": {"bound": "hbm", "achieved": round(gdn_gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                             "frac": round(gdn_gbs / HBM_PEAK_GBS, 4), "algorithmic_bytes_per_call": gdn_b,
+                             "workspace_bytes_per_call": 2 * cap.gdn_workspace_bytes(T, H)}},
         "setup_s": round(t_setup, 1),
     }
     if not args.no_cpu_baseline:

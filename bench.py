@@ -46,11 +46,14 @@ LINK_PEAK_GBS = 64.0         # host link, PCIe 5.0 x16, one direction
 # unchanged.  Summary and commands: profiles/hybrid48_hbm_traffic.md.
 MEASURED_TRAFFIC = {
     "scan_cs": {"src": "paper_2606_20537_amd/csrc/linattn_scan.hip",
-                "sha256": "6469e8dd13233581a7a272e8675453243621e36843d7ac473630a9739554b308",
-                "bytes": 1227799453},
+                "sha256": "13fc85b11900c2f2009fc3a38dc355a19d9d30fb6c47f26ae8c5ba8f4a733656",
+                "bytes": 1227929385},
     "restore": {"src": "paper_2606_20537_amd/csrc/capsule_copy.hip",
                 "sha256": "7c114eda4a9bfbb8004abca49d610710b02b7f73425ed97266d767f35e4ffc66",
-                "bytes": 1763905201},
+                "bytes": 1763895780},
+    "gdn": {"src": "paper_2606_20537_amd/csrc/gdn_scan.hip",
+            "sha256": "a97ba113fcf0c9ff667dc513194f7b3f34f31cd4f9a3fa68d76d3ab758b8c62c",
+            "bytes": 1995317035},
 }
 
 
@@ -535,7 +538,8 @@ def main():
                 "layer_ms": round(gdn_ms, 4), "tokens_per_s": round(T / (gdn_ms * 1e-3), 1),
                 "stack_tokens_per_s_36_layers": round(T / (n_lin * gdn_ms * 1e-3), 1),
                 "roofline": {"bound": "hbm", "achieved": round(gdn_gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                             "frac": round(gdn_gbs / HBM_PEAK_GBS, 4), "algorithmic_bytes_per_call": gdn_b,
+                             "frac": round(gdn_gbs / HBM_PEAK_GBS, 4), "traffic": measured_traffic("gdn"),
+                             "algorithmic_bytes_per_call": gdn_b,
                              "workspace_bytes_per_call": 2 * cap.gdn_workspace_bytes(T, H)}},
         "setup_s": round(t_setup, 1),
     }

@@ -1,11 +1,13 @@
 """A hybrid layer stack for the end-to-end GPU tests (test code).
 
-The stack owns the live buffer set of a hybrid model -- per linear-attention
-layer a recurrent state [H, dk, dv] fp32 and a conv tail [W, C] bf16, per
+The stack owns the live buffer set of a hybrid model -- per linear layer a
+recurrent state [H, dk, dv] fp32 and a conv tail [W, C] bf16, per
 full-attention layer positional K and V buffers [T_max, kv_heads, d] bf16 --
 and drives it through the library: every linear layer's prefill or decode
-step is a linattn_chunked_prefill call that reads and writes the layer's
-live state in place; snapshot / restore / fork go through the capsule calls.
+step is a linattn_chunked_prefill call (mixer "linattn") or a
+gdn_chunked_prefill call (mixer "gdn", the gated delta rule) that reads and
+writes the layer's live state in place; snapshot / restore / fork go through
+the capsule calls.
 
 What the out-of-scope parts of a model would produce is replaced by seeded
 synthetic tables (synth): the per-token q/k/v/g of each linear layer, the K/V
@@ -21,8 +23,9 @@ import synth
 
 
 class HybridStack:
-    def __init__(self, w, total_tokens, stream_seed=0, inputs=None, deploy_key=0x5EED):
+    def __init__(self, w, total_tokens, stream_seed=0, inputs=None, deploy_key=0x5EED, mixer="linattn"):
         self.w = w
+        self.mixer = mixer
         self.T_total = total_tokens
         assert total_tokens <= w.t_max
         dev = torch.device("cuda")
@@ -31,8 +34,11 @@ class HybridStack:
         seed = w.seed + 1000 * stream_seed
         # per-layer synthetic inputs over [0, total_tokens)
         if inputs is None:
-            inputs = make_inputs(w, total_tokens, seed)
+            inputs = make_inputs(w, total_tokens, seed, mixer)
         self.inp = inputs
+        self.ws = None
+        if mixer == "gdn":  # scratch of the delta-rule prefill, sized for the longest call
+            self.ws = torch.empty(max(cap.gdn_workspace_bytes(total_tokens, H), 16), dtype=torch.uint8, device=dev)
         # live buffers
         self.state = [torch.zeros((H, dk, dv), dtype=torch.float32, device=dev) for _ in range(w.n_linear)]
         cw, cc = w.conv_width, w.conv_channels
@@ -82,6 +88,12 @@ class HybridStack:
         T = t1 - t0
         for l in range(w.n_linear):
             d = self.inp["lin"][l]
+            if self.mixer == "gdn":
+                cap.gdn_chunked_prefill(d["q"][t0:t1], d["k"][t0:t1], d["v"][t0:t1], d["g"][t0:t1],
+                                        d["beta"][t0:t1], self.o[l][t0:t1], state_in=self.state[l],
+                                        final_state=self.state[l], workspace=self.ws,
+                                        T=T, H=w.heads, dk=w.dk, dv=w.dv, chunk=w.chunk)
+                continue
             cap.linattn_chunked_prefill(d["q"][t0:t1], d["k"][t0:t1], d["v"][t0:t1], d["g"][t0:t1],
                                         self.o[l][t0:t1], state_in=self.state[l], final_state=self.state[l],
                                         T=T, H=w.heads, dk=w.dk, dv=w.dv, chunk=w.chunk,
@@ -114,11 +126,14 @@ class HybridStack:
         return [t.view(torch.uint8).clone() for _, t, _, _, _ in self.bufs]
 
 
-def make_inputs(w, total_tokens, seed):
+def make_inputs(w, total_tokens, seed, mixer="linattn"):
     dev = torch.device("cuda")
     lin = []
     for l in range(w.n_linear):
-        d = synth.linattn_inputs(seed, l, total_tokens, w.heads, w.dk, w.dv, w.in_dtype)
+        if mixer == "gdn":
+            d = synth.gdn_inputs(seed, l, total_tokens, w.heads, w.dk, w.dv, w.in_dtype)
+        else:
+            d = synth.linattn_inputs(seed, l, total_tokens, w.heads, w.dk, w.dv, w.in_dtype)
         entry = {"host": d}
         for n in ("q", "k", "v"):
             pay = d[n + "_dev"]
@@ -126,6 +141,8 @@ def make_inputs(w, total_tokens, seed):
                 else torch.from_numpy(np.ascontiguousarray(pay))
             entry[n] = t.to(dev)
         entry["g"] = torch.from_numpy(d["g"]).to(dev)
+        if "beta" in d:
+            entry["beta"] = torch.from_numpy(d["beta"]).to(dev)
         lin.append(entry)
     kv = []
     for i in range(2 * w.n_full):

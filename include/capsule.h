@@ -238,7 +238,10 @@ CAP_API uint64_t capsule_digest_tokens(const int32_t* ids, uint64_t n);
  *     S_{j+1} = exp(G_last) S_j + sum_m exp(G_last - G_m) k_m^T v_m
  * The arithmetic of a chunk depends only on (S_j, that chunk's inputs): a
  * call started at a chunk-aligned position from a restored state reproduces,
- * bit for bit, what one longer call computes for the same tokens.
+ * bit for bit, what one longer call computes for the same tokens.  A call of
+ * exactly one bf16 token (a decode step) takes a shorter path whose state is
+ * bit-identical to the chunked one's and whose o may differ from it in fp32
+ * rounding only.
  *
  * Layouts (all contiguous, device, caller-owned):
  *   q, k : [T, H, dk]  in_dtype (bf16 or f32)      v : [T, H, dv] in_dtype

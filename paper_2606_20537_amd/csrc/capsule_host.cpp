@@ -621,6 +621,8 @@ int linattn_chunked_prefill(const linattn_args* a, void* stream) {
     p.in_f32 = a->in_dtype == CAP_DTYPE_F32 ? 1 : 0;
     p.scale = a->scale;
     if (a->T == 0 && !a->final_state) return CAP_OK;
+    // a one-token bf16 call (a decode step) takes the vector-ALU step kernel
+    if (a->T == 1 && !p.in_f32) return launch_status(cap::launch_linattn_step(p, static_cast<hipStream_t>(stream)));
     return launch_status(cap::launch_linattn_scan(p, static_cast<hipStream_t>(stream)));
 }
 

@@ -1,6 +1,6 @@
 // Internal interface between the host ABI (capsule_host.cpp) and the HIP
-// kernels (capsule_copy.hip, linattn_scan.hip, gdn_scan.hip, kv_fp8.hip,
-// append.hip).  Not part of the public ABI.
+// kernels (capsule_copy.hip, linattn_scan.hip, linattn_step.hip,
+// gdn_scan.hip, kv_fp8.hip, append.hip).  Not part of the public ABI.
 #pragma once
 
 #include <hip/hip_runtime_api.h>
@@ -66,6 +66,8 @@ struct ScanParams {
 };
 
 hipError_t launch_linattn_scan(const ScanParams& p, hipStream_t stream);
+// T == 1, bf16 inputs (a decode step); same contract as launch_linattn_scan
+hipError_t launch_linattn_step(const ScanParams& p, hipStream_t stream);
 
 // Gated delta-rule prefill (bf16 q/k/v, fp32 gates, write strengths and
 // state).  ws holds one record of kGdnWsRecord bytes per chunk of 64 tokens

@@ -38,6 +38,9 @@ CASES = [
     ("bf16_hybrid8_layer", 2048, 16, 128, 128, "bf16", False),
     ("bf16_one_chunk_exact", 64, 2, 128, 128, "bf16", True),
     ("bf16_one_token", 1, 2, 128, 128, "bf16", True),
+    ("bf16_one_token_dk64_oddH", 1, 3, 64, 48, "bf16", True),
+    ("bf16_one_token_zero_state", 1, 5, 128, 16, "bf16", False),
+    ("f32_one_token", 1, 2, 64, 64, "f32", True),
     ("bf16_63", 63, 2, 128, 48, "bf16", True),
     ("bf16_65", 65, 2, 128, 48, "bf16", True),
 ]
@@ -143,3 +146,49 @@ def test_aligned_continuation_bitwise(P):
     assert torch.equal(st, fs_full)
     # the chunk-boundary state output at P is the state a prefill stopping at P hands over
     assert torch.equal(st_P, cs_full[P // 64])
+
+
+@pytest.mark.parametrize("dk,dv", [(128, 128), (64, 32)])
+def test_one_token_state_equals_chunked_fold(dk, dv):
+    """A one-token call (the decode path) folds the state exactly as the
+    chunked kernel folds a one-token chunk: the state after token 64 of one
+    65-token call equals, bit for bit, a one-token call from that call's
+    chunk-boundary state 1; o of that token agrees to fp32 rounding."""
+    import torch
+    T, H = 65, 4
+    inp = scan_case(41, T, H, dk, dv)
+    S0 = np.random.default_rng(7).standard_normal((H, dk, dv)).astype(np.float32)
+    o, cs, fs = _run(inp, T, H, dk, dv, S0=S0)
+    d = dev_inputs(inp)
+    st = torch.from_numpy(cs[1]).cuda()
+    o1 = torch.empty((1, H, dv), dtype=torch.float32, device="cuda")
+    cs1 = torch.empty((1, H, dk, dv), dtype=torch.float32, device="cuda")
+    fs1 = torch.empty((H, dk, dv), dtype=torch.float32, device="cuda")
+    cap.linattn_chunked_prefill(d["q"][64:], d["k"][64:], d["v"][64:], d["g"][64:], o1, state_in=st,
+                                chunk_states=cs1, final_state=fs1, T=1, H=H, dk=dk, dv=dv,
+                                in_dtype=cap.CAP_DTYPE_BF16)
+    torch.cuda.synchronize()
+    assert np.array_equal(fs1.cpu().numpy(), fs)
+    assert np.array_equal(cs1.cpu().numpy()[0], cs[1])  # entry 0 is the state entering the call
+    assert rel_err(o1.cpu().numpy()[0], o[64]) <= SPLIT_TOL
+
+
+def test_one_token_inplace_and_optional_outputs(orc):
+    """One-token calls: final_state may be state_in; chunk_states / final_state
+    may be NULL; a NULL state_in is the zero state."""
+    import torch
+    H, dk, dv = 3, 128, 64
+    inp = scan_case(43, 1, H, dk, dv)
+    S0 = np.random.default_rng(9).standard_normal((H, dk, dv)).astype(np.float32)
+    o_a, cs_a, fs_a = _run(inp, 1, H, dk, dv, S0=S0)
+    o_b, _, _ = _run(inp, 1, H, dk, dv, S0=S0, want_cs=False, want_final=False)
+    assert np.array_equal(o_a, o_b) and np.array_equal(cs_a[0], S0)
+    d = dev_inputs(inp)
+    st = torch.from_numpy(S0).cuda()
+    o = torch.empty((1, H, dv), dtype=torch.float32, device="cuda")
+    cap.linattn_chunked_prefill(d["q"], d["k"], d["v"], d["g"], o, state_in=st, final_state=st)
+    torch.cuda.synchronize()
+    assert np.array_equal(o.cpu().numpy(), o_a) and np.array_equal(st.cpu().numpy(), fs_a)
+    o_z, cs_z, fs_z = _run(inp, 1, H, dk, dv)
+    o_ref, s_ref = orc.sequential(inp["q"], inp["k"], inp["v"], inp["g"])
+    assert not cs_z.any() and rel_err(o_z, o_ref) <= SPLIT_TOL and rel_err(fs_z, s_ref) <= SPLIT_TOL

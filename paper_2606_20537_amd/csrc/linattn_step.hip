@@ -29,8 +29,15 @@ __global__ __launch_bounds__(2 * DK) void linattn_step_kernel(const ScanParams p
     constexpr int NW = 2 * DK / 64;  // waves
     __shared__ float part[NW][2][9];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    // workgroup -> (head, slice); the slices of a head share an XCD (and its
+    // L2) when the grid allows it, since neighbouring slices read the two
+    // halves of the same 128-byte state lines (workgroups go round-robin
+    // over 8 XCDs)
     const int NS = p.dv / DVS;
-    const int h = blockIdx.x / NS, j0 = (blockIdx.x % NS) * DVS;
+    const int N = p.H * NS;
+    int logical = blockIdx.x;
+    if ((N % 8) == 0 && ((N / 8) % NS) == 0) logical = (blockIdx.x % 8) * (N / 8) + blockIdx.x / 8;
+    const int h = logical / NS, j0 = (logical % NS) * DVS;
     const int d = tid >> 1, c0 = 8 * (tid & 1);
     const int64_t sidx = ((int64_t)h * DK + d) * p.dv + j0 + c0;  // element of S[h][d][j0 + c0]
 

@@ -293,7 +293,10 @@ CAP_API int linattn_chunked_prefill(const linattn_args* args, void* stream);
  * S_new = gamma_last S + sum_m exp(G_last - G_m) k_m^T u_m.  As for the
  * linear-attention scan, a chunk's arithmetic depends only on (S, that
  * chunk's inputs): restore at an aligned position then continue equals one
- * longer call bit for bit.
+ * longer call bit for bit.  A call of exactly one token (a decode step) is
+ * one launch on a shorter path (with A = 0 and (I + A)^-1 = I) whose state
+ * and o agree with the chunked path's to fp32 rounding; it does not touch
+ * the workspace.
  *
  * Layouts (contiguous, device, caller-owned):
  *   q, k : [T, H, dk] bf16     v : [T, H, dv] bf16

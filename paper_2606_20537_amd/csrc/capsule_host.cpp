@@ -680,6 +680,8 @@ int gdn_chunked_prefill(const gdn_args* a, void* stream) {
     p.T = a->T; p.H = a->H; p.dk = a->dk; p.dv = a->dv;
     p.scale = a->scale;
     if (a->T == 0 && !a->final_state) return CAP_OK;
+    // a one-token call (a decode step) takes the single-launch step kernel
+    if (a->T == 1) return launch_status(cap::launch_gdn_step(p, static_cast<hipStream_t>(stream)));
     return launch_status(cap::launch_gdn(p, static_cast<hipStream_t>(stream)));
 }
 

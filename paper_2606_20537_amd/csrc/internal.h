@@ -1,6 +1,7 @@
 // Internal interface between the host ABI (capsule_host.cpp) and the HIP
 // kernels (capsule_copy.hip, linattn_scan.hip, linattn_step.hip,
-// gdn_scan.hip, kv_fp8.hip, append.hip).  Not part of the public ABI.
+// gdn_scan.hip, gdn_step.hip, kv_fp8.hip, append.hip).  Not part of the
+// public ABI.
 #pragma once
 
 #include <hip/hip_runtime_api.h>
@@ -98,6 +99,8 @@ struct GdnParams {
 };
 
 hipError_t launch_gdn(const GdnParams& p, hipStream_t stream);
+// T == 1 (a decode step): one launch, no workspace use
+hipError_t launch_gdn_step(const GdnParams& p, hipStream_t stream);
 
 // FP8 (OCP E4M3) conversion of up to kFp8MaxSeg segments in one launch.
 // Segment s converts n_groups[s] groups of 16 elements from src[s] to

@@ -58,6 +58,8 @@ CASES = [
     ("hybrid8_layer", 2048, 16, 128, 128, False),
     ("one_chunk_exact", 64, 2, 128, 128, True),
     ("one_token", 1, 2, 128, 128, True),
+    ("one_token_dk64_oddH", 1, 3, 64, 48, True),
+    ("one_token_zero_state", 1, 5, 128, 16, False),
     ("t63", 63, 2, 128, 48, True),
     ("t65", 65, 2, 128, 48, True),
     ("dk64_long", 1000, 2, 64, 32, True),
@@ -182,3 +184,50 @@ def test_gdn_workspace_is_caller_owned(orc):
     with pytest.raises(cap.CapsuleError) as ei:
         cap.gdn_chunked_prefill(d["q"], d["k"], d["v"], d["g"], d["beta"], o, workspace=ws, workspace_bytes=need - 16)
     assert ei.value.status == cap.CAP_E_SIZE
+
+
+@pytest.mark.parametrize("dk,dv", [(128, 128), (64, 32)])
+def test_gdn_one_token_agrees_with_chunked(dk, dv):
+    """A one-token call (the decode path, one launch) continues from a chunk
+    boundary like the chunked kernel's one-token chunk: token 64 of one
+    65-token call against a one-token call from that call's chunk state 1 --
+    state and o equal to fp32 rounding, chunk state 0 = the entering state."""
+    import torch
+    T, H = 65, 4
+    inp = gdn_case(47, T, H, dk, dv)
+    S0 = np.random.default_rng(13).standard_normal((H, dk, dv)).astype(np.float32)
+    o, cs, fs = _run(inp, T, H, dk, dv, S0=S0)
+    d = _dev(inp)
+    st = torch.from_numpy(cs[1]).cuda()
+    o1 = torch.empty((1, H, dv), dtype=torch.float32, device="cuda")
+    cs1 = torch.empty((1, H, dk, dv), dtype=torch.float32, device="cuda")
+    fs1 = torch.empty((H, dk, dv), dtype=torch.float32, device="cuda")
+    cap.gdn_chunked_prefill(d["q"][64:], d["k"][64:], d["v"][64:], d["g"][64:], d["beta"][64:], o1, state_in=st,
+                            chunk_states=cs1, final_state=fs1, T=1, H=H, dk=dk, dv=dv)
+    torch.cuda.synchronize()
+    assert np.array_equal(cs1.cpu().numpy()[0], cs[1])
+    assert rel_err(fs1.cpu().numpy(), fs) <= SPLIT_TOL
+    assert rel_err(o1.cpu().numpy()[0], o[64]) <= SPLIT_TOL
+
+
+@pytest.mark.parametrize("gv,bv", [(-100.0, None), (None, 0.0), (None, 1.0)])
+def test_gdn_one_token_extremes_and_inplace(orc, gv, bv):
+    """One-token calls at g = -100 (state wiped), beta = 0 (pure decay) and
+    beta = 1 (full replacement along k), updating the state in place."""
+    import torch
+    H, dk, dv = 3, 128, 64
+    inp = gdn_case(53, 1, H, dk, dv)
+    if gv is not None:
+        inp["g"][:] = np.float32(gv)
+    if bv is not None:
+        inp["beta"][:] = np.float32(bv)
+    S0 = np.random.default_rng(17).standard_normal((H, dk, dv)).astype(np.float32)
+    d = _dev(inp)
+    st = torch.from_numpy(S0).cuda()
+    o = torch.empty((1, H, dv), dtype=torch.float32, device="cuda")
+    cap.gdn_chunked_prefill(d["q"], d["k"], d["v"], d["g"], d["beta"], o, state_in=st, final_state=st)
+    torch.cuda.synchronize()
+    o_ref, s_ref = orc.gdn_sequential(inp["q"], inp["k"], inp["v"], inp["g"], inp["beta"], S0=S0)
+    e = (rel_err(o.cpu().numpy(), o_ref), rel_err(st.cpu().numpy(), s_ref))
+    print("  g %s beta %s: rel err o %.3g state %.3g" % ((gv, bv) + e), flush=True)
+    assert max(e) <= SPLIT_TOL, e

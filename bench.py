@@ -19,7 +19,9 @@ on.  restore/cold TTFT = (phase 2 + phase 6) / (phase 4 + phase 6).
 
 After the timed steps, one gated delta-rule layer of the same shape (the
 model family's Gated DeltaNet state; q/k/v bf16, gates and write strengths
-fp32) is timed on its own under `gdn`.
+fp32) is timed on its own under `gdn`, and the robot episode reset (32
+environments, a gallery of 8 capsules, 1000 batched gather-restores) under
+`gather`.
 
 The JSON line's `value` is the capsule restore bandwidth (GB/s, bytes read +
 written); the scan and TTFT figures ride along as extra keys.  `roofline`
@@ -467,6 +469,58 @@ def main():
     assert bool(torch.isfinite(g_o).all()) and bool(torch.isfinite(g_fs).all())
     del gd, g_o, g_cs, g_fs
 
+    # ---- robot episode reset (the gather verb), outside the timed step: 32
+    # environments, a gallery of 8 capsules (18 KV layers [816 tokens, 1 head,
+    # d=256] bf16 + a 2 MiB fp32 denoiser state each); one reset restores
+    # gallery[id_e] into environment e for every e in one launch; 1000
+    # resets back to back after 20 warm-up resets (the 137 MB gallery then
+    # sits in the Infinity Cache); the last reset is checked byte for byte
+    rw = synth.get_config("robot_reset")
+    rx = dict(rw.extra)
+    rlayout = [("kv%d.%s" % (l, nm), rw.kv_row_bytes, rw.t_max, cap.CAP_KIND_POSITIONAL)
+               for l in range(rw.n_full) for nm in ("k", "v")]
+    rlayout.append(("denoiser", rx["denoiser_bytes"], 1, cap.CAP_KIND_FIXED))
+
+    def reset_bufs(seed):
+        out_b = []
+        for i, (nm, rb, rows, kind) in enumerate(rlayout):
+            t = torch.empty(rb * rows, dtype=torch.uint8, device=dev)
+            t.view(torch.float32).normal_(generator=torch.Generator(device=dev).manual_seed(seed * 1000 + i))
+            out_b.append((nm, t, rb, rows, kind))
+        return out_b
+
+    RP = rw.prefix
+    gal_keep, gallery = [], []
+    for gi in range(rx["gallery"]):
+        b = reset_bufs(100 + gi)
+        s_g = cap.cap_set_create(b, rw.chunk, 3)
+        cap.cap_set_set_position(s_g, RP)
+        ar = torch.empty(cap.capsule_bytes(s_g, RP), dtype=torch.uint8, device=dev)
+        gallery.append(cap.capsule_snapshot(s_g, RP, 0, ar, stream=stream))
+        gal_keep.append((s_g, b, ar))
+    env_keep = [reset_bufs(500 + e) for e in range(rx["envs"])]
+    env_sets = [cap.cap_set_create(b, rw.chunk, 3) for b in env_keep]
+    gal_bytes = cap.capsule_info(gallery[0])["bytes"]
+    ids_all = synth.rng(rw.seed, 0, "reset_ids").integers(0, rx["gallery"], size=(rx["resets"], rx["envs"]))
+    ids_all = ids_all.astype(np.int32)
+    stream.synchronize()
+    with torch.cuda.stream(stream):
+        for r in range(20):
+            cap.capsule_gather_restore(gallery, ids_all[r], env_sets, stream=stream)
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        e[0].record(stream)
+        for r in range(rx["resets"]):
+            cap.capsule_gather_restore(gallery, ids_all[r], env_sets, stream=stream)
+        e[1].record(stream)
+    stream.synchronize()
+    reset_ms = e[0].elapsed_time(e[1]) / rx["resets"]
+    assert RP == rw.t_max  # every row of a K/V buffer is inside the capsule
+    for env, gi in enumerate(ids_all[-1]):
+        for (_, te, *_), (_, tg, *_) in zip(env_keep[env], gal_keep[gi][1]):
+            assert torch.equal(te, tg)
+    reset_bytes = 2 * rx["envs"] * gal_bytes  # each environment's capsule read once and written once
+    del gal_keep, gallery, env_keep, env_sets
+
     scan_b = scan_bytes(T, H, dk, dv, True)
     scan_b_final = scan_bytes(T, H, dk, dv, False)
     flops = scan_useful_flops(T, H, dk, dv)
@@ -522,7 +576,7 @@ def main():
                                  "graph_ms": round(graph_ms, 4), "speedup": round(eager_ms / graph_ms, 3),
                                  "host_enqueue_us": {"eager": round(float(np.median(enq_us["eager"])), 1),
                                                      "graph": round(float(np.median(enq_us["graph"])), 1)},
-                                 "what": "capsule restore + one token (K/V + conv append, %d one-token scans)" % n_lin},
+                                 "what": "capsule restore + one token (K/V + conv append, %d one-token steps)" % n_lin},
         "fp8_kv": {"capsule_bytes": cap8_bytes, "bf16_capsule_bytes": cap_bytes,
                    "restore_ms": round(f8ms["restore"], 4), "snapshot_ms": round(f8ms["snapshot"], 4),
                    "restore_gbs": round(2 * cap8_bytes / (f8ms["restore"] * 1e-3) / 1e9, 2),
@@ -541,6 +595,17 @@ def main():
                              "frac": round(gdn_gbs / HBM_PEAK_GBS, 4), "traffic": measured_traffic("gdn"),
                              "algorithmic_bytes_per_call": gdn_b,
                              "workspace_bytes_per_call": 2 * cap.gdn_workspace_bytes(T, H)}},
+        "gather": {"what": "robot episode reset: %d environments, gallery of %d capsules of %d B, %d resets back "
+                           "to back, one gather launch each" % (rx["envs"], rx["gallery"], gal_bytes, rx["resets"]),
+                   "reset_ms": round(reset_ms, 4), "resets_per_s": round(1e3 / reset_ms, 1),
+                   "gbs": round(reset_bytes / (reset_ms * 1e-3) / 1e9, 2),
+                   "write_gbs": round(reset_bytes / 2 / (reset_ms * 1e-3) / 1e9, 2),
+                   "roofline": {"bound": "hbm", "achieved": round(reset_bytes / (reset_ms * 1e-3) / 1e9, 2),
+                                "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                "frac": round(reset_bytes / (reset_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                                "traffic": None, "algorithmic_bytes_per_launch": reset_bytes,
+                                "note": "gallery reads are served from the Infinity Cache after warm-up; "
+                                        "the writes go to HBM"}},
         "setup_s": round(t_setup, 1),
     }
     if not args.no_cpu_baseline:

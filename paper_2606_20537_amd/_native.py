@@ -147,9 +147,7 @@ class CapSet:
         self.n = n
 
     def destroy(self):
-        if self.handle:
-            cap_set_destroy(self)
-            self.handle = None
+        cap_set_destroy(self)
 
     def __del__(self):
         try:
@@ -166,9 +164,7 @@ class Capsule:
         self.arena_ref = arena_ref  # keeps a torch arena alive while the header lives
 
     def release(self):
-        if self.handle:
-            capsule_release(self)
-            self.handle = None
+        capsule_release(self)
 
     def __del__(self):
         try:
@@ -214,7 +210,12 @@ def cap_set_create(bufs, chunk, deploy_key):
 
 
 def cap_set_destroy(s):
-    return _check("cap_set_destroy", load().cap_set_destroy(s.handle))
+    """Free the set's C handle; the handle is cleared first, so a second
+    destroy (explicit or by the garbage collector) is a no-op."""
+    h, s.handle = s.handle, None
+    if not h:
+        return CAP_OK
+    return _check("cap_set_destroy", load().cap_set_destroy(h))
 
 
 def cap_set_set_position(s, position):
@@ -299,7 +300,12 @@ def capsule_tier(cap):
 
 
 def capsule_release(cap):
-    return _check("capsule_release", load().capsule_release(cap.handle))
+    """Free the capsule's host header; the handle is cleared first, so a
+    second release (explicit or by the garbage collector) is a no-op."""
+    h, cap.handle = cap.handle, None
+    if not h:
+        return CAP_OK
+    return _check("capsule_release", load().capsule_release(h))
 
 
 def capsule_digest_tokens(ids):

@@ -175,3 +175,38 @@ def test_rollback_to_earlier_capsule():
     for got, w, (_, _, rb, rows, kind) in zip(_host(bufs), at64, bufs):
         n = 64 * rb if kind == cap.CAP_KIND_POSITIONAL else rb * rows
         assert np.array_equal(got[:n], w[:n])
+
+
+def test_explicit_release_then_collection_is_safe():
+    """Releasing a capsule (or destroying a set) through the module functions
+    and then dropping the Python object frees each C handle once: a new
+    capsule made afterwards (which may reuse the freed header's memory)
+    still restores byte for byte."""
+    import gc
+    import torch
+    s, bufs = _make_set(9)
+    cap.cap_set_set_position(s, 192)
+    nbytes = cap.capsule_bytes(s, 192)
+    arena = device_bytes(nbytes, fill=0)
+    for rnd in range(3):
+        c = cap.capsule_snapshot(s, 192, 7, arena)
+        cap.capsule_release(c)
+        assert c.handle is None
+        cap.capsule_release(c)   # a second release is a no-op
+        del c
+        gc.collect()
+    c = cap.capsule_snapshot(s, 192, 7, arena)
+    want = [b[1].clone() for b in bufs]
+    for b in bufs:
+        b[1].fill_(0x5A)
+    cap.capsule_restore(c, s, 7)
+    torch.cuda.synchronize()
+    for b, w in zip(bufs, want):
+        n = b[2] * (192 if b[4] == cap.CAP_KIND_POSITIONAL else b[3])
+        assert torch.equal(b[1][:n], w[:n]), b[0]
+    s2, _ = _make_set(10)
+    cap.cap_set_destroy(s2)
+    assert s2.handle is None
+    s2.destroy()                 # no-op
+    del s2
+    gc.collect()

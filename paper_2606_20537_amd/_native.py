@@ -139,12 +139,15 @@ def _stream(s):
 
 
 class CapSet:
-    """Handle of a live set (owns the C handle; destroy() or GC frees it)."""
+    """Handle of a live set (owns the C handle; destroy() or GC frees it).
+    The set only points at its buffers, so the handle keeps the buffer
+    objects (tensors) alive while it lives."""
 
-    def __init__(self, handle, names, n):
+    def __init__(self, handle, names, n, buffers=()):
         self.handle = handle
         self.names = names
         self.n = n
+        self.buffers = list(buffers)
 
     def destroy(self):
         cap_set_destroy(self)
@@ -206,7 +209,8 @@ def cap_set_create(bufs, chunk, deploy_key):
     h = _vp()
     _check("cap_set_create", load().cap_set_create(arr, len(arr), int(chunk), int(deploy_key) & (2**64 - 1),
                                                     ct.byref(h)))
-    return CapSet(h.value, [k.decode() if k else None for k in keep], len(arr))
+    return CapSet(h.value, [k.decode() if k else None for k in keep], len(arr),
+                  [b[1] for b in bufs if not isinstance(b[1], int)])
 
 
 def cap_set_destroy(s):

@@ -253,7 +253,8 @@ CAP_API uint64_t capsule_digest_tokens(const int32_t* ids, uint64_t n);
  *   final_state  : [H, dk, dv] fp32 or NULL; the state after the last token.
  *                  May be the same pointer as state_in (in-place update).
  * Supported: chunk == 64, dk in {64, 128} (fp32 inputs: dk == 64), dv a
- * multiple of 16, 1 <= H,
+ * multiple of 16, 1 <= H, H dk dv 4 < 2^31 and 64 H max(dk, dv) 4 < 2^31
+ * (32-bit offsets inside one state and one chunk),
  * 0 <= T; pointers 16-byte aligned; o / chunk_states / final_state must not
  * overlap the inputs (except final_state == state_in).
  * Errors: CAP_E_INVAL (null required pointer, T < 0, H < 1, bad dtype,
@@ -307,7 +308,9 @@ CAP_API int linattn_chunked_prefill(const linattn_args* args, void* stream);
  *               aligned; holds the per-chunk inverses (I + A)^-1 and gate
  *               tables during the call (contents undefined afterwards).  May
  *               be NULL when T = 0.
- * Supported: chunk == 64, dk in {64, 128}, dv a multiple of 16, bf16 inputs.
+ * Supported: chunk == 64, dk in {64, 128}, dv a multiple of 16, bf16 inputs,
+ * H dk dv 4 < 2^31 and 64 H max(dk, dv) 4 < 2^31 (32-bit offsets inside one
+ * state and one chunk).
  * Errors: CAP_E_INVAL (null required pointer, T < 0, H < 1, bad dtype,
  * overlapping buffers), CAP_E_SIZE (workspace_bytes too small),
  * CAP_E_UNSUPPORTED (shape outside the list), CAP_E_ALIGN. */

@@ -587,6 +587,13 @@ int linattn_chunked_prefill(const linattn_args* a, void* stream) {
     if (a->chunk != 64 || (a->dk != 64 && a->dk != 128) || (a->dv % 16) != 0) return CAP_E_UNSUPPORTED;
     if (a->in_dtype == CAP_DTYPE_F32 && a->dk != 64) return CAP_E_UNSUPPORTED;
     if ((int64_t)a->H * (a->dv / 16) > 0x7fffffff) return CAP_E_UNSUPPORTED;
+    // the kernels address one chunk of rows, and one state of all heads, with
+    // 32-bit byte offsets
+    {
+        const uint64_t H = (uint64_t)a->H, dk = (uint64_t)a->dk, dv = (uint64_t)a->dv;
+        if (64 * H * (dk > dv ? dk : dv) * 4 > 0x7fffffffull || H * dk * dv * 4 > 0x7fffffffull)
+            return CAP_E_UNSUPPORTED;
+    }
     if (a->T > 0 && (!a->q || !a->k || !a->v || !a->g || !a->o)) return CAP_E_INVAL;
     const uint64_t ptrs[] = {(uint64_t)(uintptr_t)a->q, (uint64_t)(uintptr_t)a->k, (uint64_t)(uintptr_t)a->v,
                              (uint64_t)(uintptr_t)a->g, (uint64_t)(uintptr_t)a->state_in,
@@ -638,10 +645,12 @@ int gdn_chunked_prefill(const gdn_args* a, void* stream) {
     if (a->in_dtype != CAP_DTYPE_BF16 && a->in_dtype != CAP_DTYPE_F32) return CAP_E_INVAL;
     if (a->in_dtype != CAP_DTYPE_BF16) return CAP_E_UNSUPPORTED;
     if (a->chunk != 64 || (a->dk != 64 && a->dk != 128) || (a->dv % 16) != 0) return CAP_E_UNSUPPORTED;
-    // 32-bit offsets inside one chunk of q / k / v / o rows, and grid sizes
+    // 32-bit offsets inside one chunk of q / k / v / o rows and inside one
+    // state of all heads, and grid sizes
     const uint64_t T = (uint64_t)a->T, H = (uint64_t)a->H, dk = (uint64_t)a->dk, dv = (uint64_t)a->dv;
     const uint64_t nck = (T + 63) / 64;
-    if (64 * H * (dk > dv ? dk : dv) * 4 > 0x7fffffffull) return CAP_E_UNSUPPORTED;
+    if (64 * H * (dk > dv ? dk : dv) * 4 > 0x7fffffffull || H * dk * dv * 4 > 0x7fffffffull)
+        return CAP_E_UNSUPPORTED;
     if (H * (dv / 16) > 0x7fffffffull || nck * H > 0x7fffffffull) return CAP_E_UNSUPPORTED;
     if (a->T > 0 && (!a->q || !a->k || !a->v || !a->g || !a->beta || !a->o || !a->workspace)) return CAP_E_INVAL;
     const uint64_t ws_need = gdn_workspace_bytes(a->T, a->H, a->chunk);

@@ -156,6 +156,9 @@ def test_scan_argument_checks():
     assert _scan_status(final_state=1 << 30) == cap.CAP_E_INVAL
     # nothing to do: T = 0 without a final state returns at once
     assert _scan_status(T=0, q=0, k=0, v=0, g=0, o=0) == cap.CAP_OK
+    # more heads than 32-bit offsets inside one state of all heads can address
+    assert _scan_status(H=32768, dk=128, dv=128) == cap.CAP_E_UNSUPPORTED
+    assert _scan_status(H=32767, dk=128, dv=128, T=0, q=0, k=0, v=0, g=0, o=0) == cap.CAP_OK
 
 
 def _gdn_status(**kw):
@@ -189,6 +192,8 @@ def test_gdn_argument_checks():
     assert _gdn_status(o=12288 + 32) == cap.CAP_E_INVAL
     # nothing to do: T = 0 without a final state returns at once, no workspace needed
     assert _gdn_status(T=0, q=0, k=0, v=0, g=0, beta=0, o=0, workspace=0, workspace_bytes=0) == cap.CAP_OK
+    # more heads than 32-bit offsets inside one state of all heads can address
+    assert _gdn_status(H=32768, dk=128, dv=128) == cap.CAP_E_UNSUPPORTED
 
 
 def test_python_binding_has_no_fallback(tmp_path):

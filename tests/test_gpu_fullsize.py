@@ -172,3 +172,63 @@ def test_robot_reset_1000_gather_restores():
                 for (name, t, rb, rows, kind), src in zip(b, gal_bufs[i][1]):
                     assert torch.equal(t, src[1]), (r, name)
     assert int(mismatches) == 0
+
+
+def test_long_sequence_131072_tokens(orc):
+    """131,072 tokens in one call (2048 chunks; chunk-state offsets past
+    4 GiB, 64-bit chunk bases): o and the final state against the oracle's
+    recurrence on every head, and the chunk state entering the last chunk
+    equal, bit for bit, to the final state of a call over the first 2047
+    chunks."""
+    T, H, dk, dv = 131072, 2, 128, 128
+    inp = synth.linattn_inputs(H48.seed + 3, 0, T, H, dk, dv, "bf16")
+    d = dev_inputs(inp)
+    n_chunks = T // 64
+    o = torch.empty((T, H, dv), dtype=torch.float32, device="cuda")
+    cs = torch.empty((n_chunks, H, dk, dv), dtype=torch.float32, device="cuda")
+    fs = torch.empty((H, dk, dv), dtype=torch.float32, device="cuda")
+    print("one call over %d tokens" % T, flush=True)
+    cap.linattn_chunked_prefill(d["q"], d["k"], d["v"], d["g"], o, chunk_states=cs, final_state=fs)
+    Tp = T - 64
+    o_p = torch.empty((Tp, H, dv), dtype=torch.float32, device="cuda")
+    fs_p = torch.empty((H, dk, dv), dtype=torch.float32, device="cuda")
+    cap.linattn_chunked_prefill(d["q"][:Tp], d["k"][:Tp], d["v"][:Tp], d["g"][:Tp], o_p, final_state=fs_p,
+                                T=Tp, H=H, dk=dk, dv=dv, in_dtype=cap.CAP_DTYPE_BF16)
+    torch.cuda.synchronize()
+    assert torch.equal(cs[n_chunks - 1], fs_p)
+    assert torch.equal(o[:Tp], o_p)
+    print("oracle recurrence over %d tokens x %d heads" % (T, H), flush=True)
+    o_ref, s_ref = orc.sequential(inp["q"], inp["k"], inp["v"], inp["g"])
+    e_o, e_s = rel_err(o.cpu().numpy(), o_ref), rel_err(fs.cpu().numpy(), s_ref)
+    print("rel err o %.3g final %.3g" % (e_o, e_s), flush=True)
+    assert e_o <= SPLIT_TOL and e_s <= SPLIT_TOL
+
+
+def test_capsule_larger_than_4gib():
+    """A 5.4 GB capsule (one positional buffer of 1,048,576 valid rows of
+    5120 B, then a fixed 2 MiB buffer whose capsule offset lies past 4 GiB):
+    snapshot and restore are byte-exact."""
+    rb, rows, P = 5120, (1 << 20) + 64, 1 << 20
+    big = torch.empty(rb * rows, dtype=torch.uint8, device="cuda")
+    big.view(torch.int32).random_(generator=torch.Generator(device="cuda").manual_seed(5))
+    st = torch.empty(2 << 20, dtype=torch.uint8, device="cuda")
+    st.view(torch.int32).random_(generator=torch.Generator(device="cuda").manual_seed(6))
+    bufs = [("kv", big, rb, rows, cap.CAP_KIND_POSITIONAL), ("state", st, 2 << 20, 1, cap.CAP_KIND_FIXED)]
+    s = cap.cap_set_create(bufs, 64, 9)
+    cap.cap_set_set_position(s, P)
+    nbytes = cap.capsule_bytes(s, P)
+    assert nbytes == rb * P + (2 << 20) and nbytes > (4 << 30)
+    arena = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    c = cap.capsule_snapshot(s, P, 3, arena)
+    torch.cuda.synchronize()
+    assert torch.equal(arena[: rb * P], big[: rb * P])
+    assert torch.equal(arena[rb * P:], st)
+    want_tail = big[rb * P:].clone()
+    big.fill_(0xA5)
+    st.fill_(0x5A)
+    cap.capsule_restore(c, s, 3)
+    torch.cuda.synchronize()
+    assert torch.equal(big[: rb * P], arena[: rb * P])
+    assert torch.equal(st, arena[rb * P:])
+    assert bool((big[rb * P:] == 0xA5).all())  # rows past P' are left alone
+    del want_tail

@@ -54,8 +54,8 @@ MEASURED_TRAFFIC = {
                 "sha256": "7c114eda4a9bfbb8004abca49d610710b02b7f73425ed97266d767f35e4ffc66",
                 "bytes": 1763895780},
     "gdn": {"src": "paper_2606_20537_amd/csrc/gdn_scan.hip",
-            "sha256": "a97ba113fcf0c9ff667dc513194f7b3f34f31cd4f9a3fa68d76d3ab758b8c62c",
-            "bytes": 1995317035},
+            "sha256": "7793817bb93174accbb7982128d2d941343977fe70c772fbe1f90a1cae78e346",
+            "bytes": 1619575466},
 }
 
 
@@ -588,7 +588,7 @@ def main():
                    "capsule_ttft_ms": round(f8ms["restore"] + f8ms["rebuild"] + ms["continue"], 4),
                    "capsule_ttft_ms_lazy_none": round(f8ms["restore"] + ms["continue"], 4)},
         "gdn": {"what": "gated delta-rule prefill, one layer (H=%d, dk=dv=%d, %d tokens, chunk states): "
-                        "(I + A)^-1 and scores launch + scan launch" % (H, dk, T),
+                        "(I + A)^-1 launch + scan launch" % (H, dk, T),
                 "layer_ms": round(gdn_ms, 4), "tokens_per_s": round(T / (gdn_ms * 1e-3), 1),
                 "stack_tokens_per_s_36_layers": round(T / (n_lin * gdn_ms * 1e-3), 1),
                 "roofline": {"bound": "hbm", "achieved": round(gdn_gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",

@@ -335,9 +335,9 @@ typedef struct gdn_args {
     float        scale;
 } gdn_args;
 
-/* Workspace size for gdn_chunked_prefill: ceil(T / 64) * H * 25088 bytes
- * (per chunk and head: the chunk's (I + A)^-1 and decayed scores in operand form and its gate
- * tables); 0 for T <= 0, H < 1 or chunk != 64. */
+/* Workspace size for gdn_chunked_prefill: ceil(T / 64) * H * 12800 bytes
+ * (per chunk and head: the chunk's (I + A)^-1 in operand form and its gate tables);
+ * 0 for T <= 0, H < 1 or chunk != 64. */
 CAP_API uint64_t gdn_workspace_bytes(int64_t T, int32_t H, int32_t chunk);
 
 CAP_API int gdn_chunked_prefill(const gdn_args* args, void* stream);

@@ -16,11 +16,10 @@
 //
 // Two launches.
 //  1. gdn_prepare, one wave per (chunk, head), all chunks in parallel: A from
-//     K K^T on MFMA, T = (I + A)^-1 by forward substitution in fp32 (lane j
-//     owns column j), and the decayed scores P = exp(G_i - G_m)(q_i . k_m),
-//     m <= i, on MFMA; both go to the workspace as ready MFMA operands.  T
-//     and P depend on the chunk's inputs only -- not on S -- and are the same
-//     for every value slice of the head, so they are computed once, off the
+//     K K^T on MFMA and T = (I + A)^-1 by forward substitution in fp32 (lane
+//     j owns column j), written to the workspace as ready MFMA operands.  T
+//     depends on the chunk's inputs only -- not on S -- and is the same for
+//     every value slice of the head, so it is computed once, off the
 //     sequential path.
 //  2. gdn_scan, one workgroup of eight waves per (head, 16-column slice of
 //     the values), walks the chunks in order.  Column slices are
@@ -28,17 +27,22 @@
 //     v[:, J].  Only K S -> R -> U -> S is a true recurrence; it runs on
 //     four "chain" waves (row block r of the chunk, rows of S), with three
 //     LDS barriers per chunk:
-//       phase 1  R_r = beta (V_r - gamma K_r S) -> LDS, and gamma Q_r S
-//                (the same S operands) for the output role
+//       phase 1  R_r = beta (V_r - gamma K_r S) -> LDS
 //       phase 2  U_r = sum_m T[r rows][m] R_m -> LDS, with w_m U_m
 //       phase 3  S <- gamma_last S + K^T (w U) on the wave's rows of S,
 //                published for the next chunk.
-//     Four "output" waves do the rest beside it: the HBM loads (three
-//     chunks ahead) and the cooperative L2 prefetch (phase 1), staging the
-//     next chunk's K and gate tables (phase 2), and o_r = scale (gamma Q_r S
-//     + P U) (phase 3).  The arithmetic applied to a chunk depends only on
-//     (S, that chunk's inputs), so a call started at an aligned position from
-//     a restored state reproduces one longer call bit for bit.
+//     Four "output" waves do the rest beside it: the HBM loads of K, Q and
+//     the gate tables (three chunks ahead) and the cooperative L2 prefetch,
+//     then gamma Q_r S (from the published S) and the decayed scores
+//     P = exp(G_i - G_m)(q_i . k_m), m <= i, of their rows (phase 1),
+//     staging the next chunk's K and gate tables (phase 2), and
+//     o_r = scale (gamma Q_r S + P U) (phase 3).  The scores are recomputed
+//     by every value slice of a head rather than read from the workspace:
+//     the slices already hold the chunk's Q and K, and the scan is bound by
+//     the lines each workgroup asks L2 for, not by its arithmetic.  The
+//     arithmetic applied to a chunk depends only on (S, that chunk's
+//     inputs), so a call started at an aligned position from a restored
+//     state reproduces one longer call bit for bit.
 //
 // Every product runs on v_mfma_f32_16x16x32_bf16 with fp32 accumulation.
 // K and Q are exact bf16 operands; fp32 operands (S, R, U, w U, T, P) are
@@ -66,22 +70,17 @@ typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 __device__ inline float f32_of(uint32_t u) { return __builtin_bit_cast(float, u); }
 
 // ------------------------------------------------------------------ prepare
-// One wave per (chunk c, head h): T = (I + A)^-1, the decayed scores
-// P = exp(G_i - G_m) (q_i . k_m) (m <= i) and the gate tables into the
-// workspace record of (c, h).  Rows past the last token have q = k = 0,
-// beta = 0 and g = 0, so their rows and columns of A and P vanish and T is
-// the identity there.  T and P do not depend on the state and are the same
-// for every value slice of the head.
+// One wave per (chunk c, head h): T = (I + A)^-1 and the gate tables into
+// the workspace record of (c, h).  Rows past the last token have k = 0,
+// beta = 0 and g = 0, so their rows and columns of A vanish and T is the
+// identity there.  T does not depend on the state and is the same for every
+// value slice of the head.
 //
-// Record layout (the scan's wave for row block r reads block (r, i) of T and
-// of P for i <= r / 2): block (r, i) = index r for r < 2, else 2 r - 2 + i;
+// Record layout (the scan's chain wave for row block r reads block (r, i)
+// for i <= r / 2): block (r, i) = index r for r < 2, else 2 r - 2 + i;
 // 2 KiB each, the bf16 hi plane then the lo plane, lane l = 16 grp + li at
-// byte 16 l of its plane holding
-//   T: T[16 r + li][32 i + 8 grp + e],                 e = 0..7
-//   P: P[16 r + li][32 i + 16 (e / 4) + 4 grp + e % 4], e = 0..7
-// (P in the accumulator layout of K_s Q_r^T, which the scan uses as is as
-// the A operand of P U).  Six T blocks, six P blocks, then G log2(e)
-// (64 fp32) and beta (64 fp32).
+// byte 16 l of its plane holding T[16 r + li][32 i + 8 grp + e], e = 0..7.
+// Six blocks, then G log2(e) (64 fp32) and beta (64 fp32).
 template <int DK>
 __global__ __launch_bounds__(64) void gdn_prepare_kernel(const GdnParams p) {
     constexpr int NKK = DK / 32;
@@ -105,14 +104,6 @@ __global__ __launch_bounds__(64) void gdn_prepare_kernel(const GdnParams p) {
         for (int kk = 0; kk < NKK; ++kk)
             kr[r][kk] = __builtin_amdgcn_raw_buffer_load_b128(
                 rk, (uint32_t)((16 * r + li) * krow + ((int64_t)h * DK + 32 * kk + 8 * grp) * 2), 0, 0);
-    const rsrc_t rq = make_rsrc(static_cast<const char*>(p.q) + t0 * krow, rows * krow);
-    u32x4 qr[4][NKK];  // same layout for the queries
-    #pragma unroll
-    for (int r = 0; r < 4; ++r)
-        #pragma unroll
-        for (int kk = 0; kk < NKK; ++kk)
-            qr[r][kk] = __builtin_amdgcn_raw_buffer_load_b128(
-                rq, (uint32_t)((16 * r + li) * krow + ((int64_t)h * DK + 32 * kk + 8 * grp) * 2), 0, 0);
     const rsrc_t rg = make_rsrc(p.g + t0 * H, rows * H * 4);
     const rsrc_t rb = make_rsrc(p.beta + t0 * H, rows * H * 4);
     const float gl = f32_of(__builtin_amdgcn_raw_buffer_load_b32(rg, (uint32_t)((lane * H + h) * 4), 0, 0));
@@ -142,39 +133,7 @@ __global__ __launch_bounds__(64) void gdn_prepare_kernel(const GdnParams p) {
         }
     }
 
-    // P blocks: tile (r, s) = K_s Q_r^T holds P[16 r + li][16 s + 4 grp + q]
-    // in lane (grp, li), element q
     uint8_t* rec = p.ws + (c * H + h) * kGdnWsRecord;
-    #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const float gi = tg[16 * r + li];
-        #pragma unroll
-        for (int i = 0; i <= r / 2; ++i) {
-            float f[8];
-            #pragma unroll
-            for (int half = 0; half < 2; ++half) {
-                const int s = 2 * i + half;
-                if (s > r) {
-                    #pragma unroll
-                    for (int q = 0; q < 4; ++q) f[4 * half + q] = 0.0f;
-                    continue;
-                }
-                f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-                #pragma unroll
-                for (int kk = 0; kk < NKK; ++kk)
-                    acc = mma(__builtin_bit_cast(bf16x8, kr[s][kk]), __builtin_bit_cast(bf16x8, qr[r][kk]), acc);
-                const f32x4 gm = *reinterpret_cast<const f32x4*>(&tg[16 * s + 4 * grp]);
-                #pragma unroll
-                for (int q = 0; q < 4; ++q)
-                    f[4 * half + q] = (s < r || 4 * grp + q <= li) ? acc[q] * exp2f(gi - gm[q]) : 0.0f;
-            }
-            bf16x8 hi, lo;
-            split_n<8>(f, hi, lo);
-            const int blk = r < 2 ? r : 2 * r - 2 + i;
-            *reinterpret_cast<bf16x8*>(rec + kGdnWsPOff + blk * 2048 + 16 * lane) = hi;
-            *reinterpret_cast<bf16x8*>(rec + kGdnWsPOff + blk * 2048 + 1024 + 16 * lane) = lo;
-        }
-    }
     __syncthreads();
 
     // column `lane` of T: x_t = [t == lane] - sum_{m<t} A_tm x_m, applied
@@ -235,7 +194,6 @@ struct alignas(16) GdnSmem {
     alignas(16) __bf16 u[2][CH * JP];     // U [m][j]: hi, lo
     alignas(16) __bf16 wu[2][CH * JP];    // w U [m][j], w_m = exp(G_last - G_m): hi, lo
     alignas(16) float tab[2][2 * CH];     // by chunk parity: G_m log2(e) (0..63), beta_m (64..127)
-    alignas(16) float x[NW][64 * 4];      // (gamma Q_r S)^T per row block, accumulator layout (lane order)
 };
 
 struct GdnCtx {
@@ -263,16 +221,18 @@ struct GdnCtx {
 // runs the step once, without prefetch.
 
 // ------------------------------------------------------------ output role
-// Wave R owns rows 16 R..16 R + 15 of the chunk: o^T = scale ((gamma X)^T +
-// U^T P^T) (phase 3) with (gamma X)^T from the chain role and P from the
-// workspace.  The role also loads K (all rows) and stages it in LDS, wave 0
-// stages the gate tables and waves 1 and 2 run the cooperative L2 prefetch.
+// Wave R owns rows i = 16 R..16 R + 15 of the chunk: in phase 1 it forms
+// (gamma X)^T = (gamma Q_R S)^T from the published S and the decayed scores
+// of its rows, P^T = (K Q_R^T) o exp(G_i - G_m) (m <= i), whose accumulators
+// serve as they are as the B operand of U^T P^T; in phase 3,
+// o^T = scale ((gamma X)^T + U^T P^T).  The role also loads K (all rows) and
+// stages it in LDS, wave 0 stages the gate tables and waves 1 and 2 run the
+// cooperative L2 prefetch.
 template <int DK, int R>
 struct OutStage {
     static constexpr int PK = CH * DK / 8 / NO_T;  // 16-byte K pieces per thread
-    static constexpr int NT2 = R / 2 + 1;
     u32x4 kp[PK];       // K pieces, coalesced (consecutive threads: consecutive bytes of a row)
-    u32x4 p[NT2][2];    // P operand blocks (R, i): bf16 hi, lo
+    u32x4 q[DK / 32];   // q[16 R + li][32 kk + 8 grp .. +7]
     float tab[2];       // wave 0: entries 2 lane, 2 lane + 1 of the gate tables
 };
 
@@ -280,7 +240,8 @@ template <int DK, bool ONE, int R>
 __device__ __forceinline__ void out_role(const GdnParams& p, GdnSmem<DK>& sm, const GdnCtx& x) {
     using Sm = GdnSmem<DK>;
     using St = OutStage<DK, R>;
-    constexpr int KP = Sm::KP, JP = Sm::JP, PK = St::PK, NT2 = St::NT2;
+    constexpr int KP = Sm::KP, JP = Sm::JP, PK = St::PK;
+    constexpr int NKK = DK / 32, NT2 = R / 2 + 1;
     const int lane = x.lane, li = x.li, grp = x.grp, h = x.h, j0 = x.j0, H = x.H, dv = x.dv;
     const int ot = 64 * R + lane;
 
@@ -293,16 +254,13 @@ __device__ __forceinline__ void out_role(const GdnParams& p, GdnSmem<DK>& sm, co
             const int m = pc / (DK / 8), d0 = (pc % (DK / 8)) * 8;
             S_.kp[u] = __builtin_amdgcn_raw_buffer_load_b128(rk, (uint32_t)(m * x.qk_row + ((int64_t)h * DK + d0) * 2), 0, 0);
         }
+        const rsrc_t rq = make_rsrc(static_cast<const char*>(p.q) + t0 * x.qk_row, rows * x.qk_row);
+        #pragma unroll
+        for (int kk = 0; kk < NKK; ++kk)
+            S_.q[kk] = __builtin_amdgcn_raw_buffer_load_b128(
+                rq, (uint32_t)((16 * R + li) * x.qk_row + ((int64_t)h * DK + 32 * kk + 8 * grp) * 2), 0, 0);
         const bool live = c < x.n;
         const uint8_t* rec = p.ws + (live ? (c * H + h) * kGdnWsRecord : 0);
-        const rsrc_t rp = make_rsrc(rec + kGdnWsPOff, live ? kGdnWsTabOff - kGdnWsPOff : 0);
-        #pragma unroll
-        for (int i = 0; i < NT2; ++i) {
-            const int blk = R < 2 ? R : 2 * R - 2 + i;
-            #pragma unroll
-            for (int pl = 0; pl < 2; ++pl)
-                S_.p[i][pl] = __builtin_amdgcn_raw_buffer_load_b128(rp, (uint32_t)(blk * 2048 + pl * 1024 + 16 * lane), 0, 0);
-        }
         if constexpr (R == 0) {
             const rsrc_t rt = make_rsrc(rec + kGdnWsTabOff, live ? 2 * CH * 4 : 0);
             const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(rt, (uint32_t)(8 * lane), 0, 0);
@@ -364,30 +322,81 @@ __device__ __forceinline__ void out_role(const GdnParams& p, GdnSmem<DK>& sm, co
     auto step = [&](int64_t c, const St& cur, const St& nxt, St& ld, int slot) {
         const bool live = c < x.n;
         const int b = (int)(c & 1);
+        const __bf16* kb = sm.k[b];
         const int64_t t0 = c * CH, rows = x.T - t0;
         if constexpr (!ONE) load(ld, c + 3);
         if constexpr (!ONE && (R == 1 || R == 2)) prefetch(slot, c + PREFETCH);
-        // ---- phase 1: nothing but the loads above (the chain computes gamma X)
+
+        // ---- phase 1: (gamma X)^T = (gamma Q_R S)^T from the published S
+        // (element e of the S^T operand of step kk is d = 32 kk + 8 grp + e),
+        // and the scores K Q_R^T: accumulator mb holds (k_m . q_i) for
+        // m = 16 mb + 4 grp + r, i = 16 R + li
+        bf16x8 qo[NKK];
+        #pragma unroll
+        for (int kk = 0; kk < NKK; ++kk) qo[kk] = __builtin_bit_cast(bf16x8, cur.q[kk]);
+        f32x4 xh = {0.f, 0.f, 0.f, 0.f}, xl = {0.f, 0.f, 0.f, 0.f};
+        #pragma unroll
+        for (int kk = 0; kk < NKK; ++kk) {
+            const int d0 = 32 * kk + 8 * grp;
+            const bf16x8 sh = cat(tr4(sm.s[0], JP, d0, 0, li), tr4(sm.s[0], JP, d0 + 4, 0, li));
+            const bf16x8 sl = cat(tr4(sm.s[1], JP, d0, 0, li), tr4(sm.s[1], JP, d0 + 4, 0, li));
+            xh = mma(sh, qo[kk], xh);
+            xl = mma(sl, qo[kk], xl);
+        }
+        f32x4 sc[R + 1];
+        #pragma unroll
+        for (int mb = 0; mb <= R; ++mb) {
+            sc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+            #pragma unroll
+            for (int kk = 0; kk < NKK; ++kk)
+                sc[mb] = mma(*reinterpret_cast<const bf16x8*>(&kb[(16 * mb + li) * KP + 32 * kk + 8 * grp]), qo[kk],
+                             sc[mb]);
+        }
+        // P^T = scores o exp(G_i - G_m) for m <= i, as the B operand of
+        // U^T P^T: element e of step i2 is m = 32 i2 + 16 (e / 4) + 4 grp + e % 4
+        const float g2i = sm.tab[b][16 * R + li];
+        bf16x8 ph[NT2], pl[NT2];
+        #pragma unroll
+        for (int i2 = 0; i2 < NT2; ++i2) {
+            float f[8];
+            #pragma unroll
+            for (int half = 0; half < 2; ++half) {
+                const int mb = 2 * i2 + half;
+                if (mb > R) {
+                    #pragma unroll
+                    for (int q = 0; q < 4; ++q) f[4 * half + q] = 0.0f;
+                    continue;
+                }
+                const f32x4 gm = *reinterpret_cast<const f32x4*>(&sm.tab[b][16 * mb + 4 * grp]);
+                #pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    f[4 * half + q] = (mb < R || 4 * grp + q <= li) ? sc[mb][q] * exp2f(g2i - gm[q]) : 0.0f;
+            }
+            split_n<8>(f, ph[i2], pl[i2]);
+        }
+        f32x4 oa;
+        {
+            const float gam = exp2f(g2i);
+            #pragma unroll
+            for (int q = 0; q < 4; ++q) oa[q] = gam * (xh[q] + xl[q]);
+        }
         if (live) lds_barrier();
 
         // ---- phase 2: stage chunk c+1
         if constexpr (!ONE) stage(nxt, b ^ 1);
-        f32x4 oa = *reinterpret_cast<const f32x4*>(&sm.x[R][4 * lane]);
         if (live) lds_barrier();
 
         // ---- phase 3: o^T = scale ((gamma X)^T + U^T P^T); element e of the
         // U^T operand of step i2 is m = 32 i2 + 16 (e / 4) + 4 grp + e % 4, the
-        // order of the P blocks
+        // order of the P^T operand
         #pragma unroll
         for (int i2 = 0; i2 < NT2; ++i2) {
-            const bf16x8 ph = __builtin_bit_cast(bf16x8, cur.p[i2][0]);
-            const bf16x8 pl = __builtin_bit_cast(bf16x8, cur.p[i2][1]);
             const int m0 = 32 * i2 + 4 * grp;
             const bf16x8 uh = cat(tr4(sm.u[0], JP, m0, 0, li), tr4(sm.u[0], JP, m0 + 16, 0, li));
             const bf16x8 ul = cat(tr4(sm.u[1], JP, m0, 0, li), tr4(sm.u[1], JP, m0 + 16, 0, li));
-            oa = mma(uh, ph, oa);
-            oa = mma(ul, ph, oa);
-            oa = mma(uh, pl, oa);
+            oa = mma(uh, ph[i2], oa);
+            oa = mma(ul, ph[i2], oa);
+            oa = mma(uh, pl[i2], oa);
         }
         const rsrc_t ro = make_rsrc(static_cast<char*>(static_cast<void*>(p.o)) + t0 * x.o_row, rows * x.o_row);
         f32x4 os;
@@ -430,7 +439,6 @@ template <int DK, int R>
 struct ChainStage {
     static constexpr int NT2 = R / 2 + 1;
     u32x4 t[NT2][2];    // T[16 R + li][32 i + 8 grp .. +7]: bf16 hi, lo
-    u32x4 q[DK / 32];   // q[16 R + li][32 kk + 8 grp .. +7]
     u32x2 v;            // bf16 v[16 R + li][j0 + 4 grp .. +3]
 };
 
@@ -457,11 +465,6 @@ __device__ __forceinline__ void chain_role(const GdnParams& p, GdnSmem<DK>& sm, 
         const rsrc_t rv = make_rsrc(static_cast<const char*>(p.v) + t0 * x.v_row, rows * x.v_row);
         S_.v = __builtin_amdgcn_raw_buffer_load_b64(
             rv, (uint32_t)((16 * R + li) * x.v_row + ((int64_t)h * dv + j0 + 4 * grp) * 2), 0, 0);
-        const rsrc_t rq = make_rsrc(static_cast<const char*>(p.q) + t0 * x.qk_row, rows * x.qk_row);
-        #pragma unroll
-        for (int kk = 0; kk < NKK; ++kk)
-            S_.q[kk] = __builtin_amdgcn_raw_buffer_load_b128(
-                rq, (uint32_t)((16 * R + li) * x.qk_row + ((int64_t)h * DK + 32 * kk + 8 * grp) * 2), 0, 0);
         const bool live = c < x.n;
         const rsrc_t rt = make_rsrc(p.ws + (live ? (c * H + h) * kGdnWsRecord : 0), live ? kGdnWsTBytes : 0);
         #pragma unroll
@@ -508,31 +511,22 @@ __device__ __forceinline__ void chain_role(const GdnParams& p, GdnSmem<DK>& sm, 
         const uint32_t v0 = cur.v[0], v1 = cur.v[1];
         const float vv[4] = {f32_of(v0 << 16), f32_of(v0 & 0xFFFF0000u), f32_of(v1 << 16), f32_of(v1 & 0xFFFF0000u)};
 
-        // ---- phase 1: R^T = beta (V - gamma K_R S_c)^T, and (gamma Q_R S_c)^T for
-        // the output role (element e of the S^T operand of step kk is
-        // d = 32 kk + 8 grp + e)
+        // ---- phase 1: R^T = beta (V - gamma K_R S_c)^T (element e of the S^T
+        // operand of step kk is d = 32 kk + 8 grp + e)
         f32x4 kh = {0.f, 0.f, 0.f, 0.f}, kl = {0.f, 0.f, 0.f, 0.f};
-        f32x4 xh = {0.f, 0.f, 0.f, 0.f}, xl = {0.f, 0.f, 0.f, 0.f};
         #pragma unroll
         for (int kk = 0; kk < NKK; ++kk) {
             const int d0 = 32 * kk + 8 * grp;
             const bf16x8 sh = cat(tr4(sm.s[0], JP, d0, 0, li), tr4(sm.s[0], JP, d0 + 4, 0, li));
             const bf16x8 sl = cat(tr4(sm.s[1], JP, d0, 0, li), tr4(sm.s[1], JP, d0 + 4, 0, li));
             const bf16x8 ko = *reinterpret_cast<const bf16x8*>(&kb[(16 * R + li) * KP + d0]);
-            const bf16x8 qo = __builtin_bit_cast(bf16x8, cur.q[kk]);
             kh = mma(sh, ko, kh);
             kl = mma(sl, ko, kl);
-            xh = mma(sh, qo, xh);
-            xl = mma(sl, qo, xl);
         }
         // the next chunk's loads go after this phase's LDS reads, so a full
         // memory pipeline cannot hold those reads back
         if constexpr (!ONE) load(ld, c + 1);
         {
-            f32x4 xg;
-            #pragma unroll
-            for (int q = 0; q < 4; ++q) xg[q] = gam * (xh[q] + xl[q]);
-            *reinterpret_cast<f32x4*>(&sm.x[R][4 * x.lane]) = xg;
             float rr[4];
             #pragma unroll
             for (int q = 0; q < 4; ++q) rr[q] = bt * (vv[q] - gam * (kh[q] + kl[q]));

@@ -73,13 +73,11 @@ hipError_t launch_linattn_step(const ScanParams& p, hipStream_t stream);
 // Gated delta-rule prefill (bf16 q/k/v, fp32 gates, write strengths and
 // state).  ws holds one record of kGdnWsRecord bytes per chunk of 64 tokens
 // and head ([n_chunks][H]), written by the first launch and read by the
-// scan: the causal blocks of the chunk's (I + A)^-1 and of its decayed
-// scores P as bf16 hi/lo MFMA operands (6 blocks x 2 KiB each, in the scan's
-// lane order), then G log2(e) (64 fp32, inclusive in-chunk log-gate sums)
-// and beta (64 fp32).
+// scan: the causal blocks of the chunk's (I + A)^-1 as bf16 hi/lo MFMA
+// operands (6 blocks x 2 KiB, in the scan's lane order), then G log2(e) (64
+// fp32, inclusive in-chunk log-gate sums) and beta (64 fp32).
 constexpr int64_t kGdnWsTBytes = 6 * 2048;
-constexpr int64_t kGdnWsPOff = kGdnWsTBytes;
-constexpr int64_t kGdnWsTabOff = kGdnWsPOff + 6 * 2048;
+constexpr int64_t kGdnWsTabOff = kGdnWsTBytes;
 constexpr int64_t kGdnWsRecord = kGdnWsTabOff + 2 * 64 * 4;
 
 struct GdnParams {

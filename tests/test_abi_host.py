@@ -163,7 +163,7 @@ def test_scan_argument_checks():
 
 def _gdn_status(**kw):
     base = dict(q=4096, k=8192, v=12288, g=16384, beta=20480, state_in=0, o=1 << 30, chunk_states=0,
-                final_state=0, workspace=1 << 31, workspace_bytes=25088, T=4, H=1, dk=64, dv=16, chunk=64,
+                final_state=0, workspace=1 << 31, workspace_bytes=12800, T=4, H=1, dk=64, dv=16, chunk=64,
                 in_dtype=cap.CAP_DTYPE_BF16, scale=1.0)
     base.update(kw)
     return N.load().gdn_chunked_prefill(ct.byref(N.gdn_args(**base)), None)
@@ -172,7 +172,7 @@ def _gdn_status(**kw):
 def test_gdn_argument_checks():
     L = N.load()
     assert L.gdn_chunked_prefill(None, None) == cap.CAP_E_INVAL
-    assert L.gdn_workspace_bytes(0, 4, 64) == 0 and L.gdn_workspace_bytes(65, 3, 64) == 2 * 3 * 25088
+    assert L.gdn_workspace_bytes(0, 4, 64) == 0 and L.gdn_workspace_bytes(65, 3, 64) == 2 * 3 * 12800
     assert L.gdn_workspace_bytes(65, 3, 32) == 0
     assert _gdn_status(T=-1) == cap.CAP_E_INVAL
     assert _gdn_status(H=0) == cap.CAP_E_INVAL
@@ -183,7 +183,7 @@ def test_gdn_argument_checks():
     assert _gdn_status(chunk=32) == cap.CAP_E_UNSUPPORTED
     assert _gdn_status(dk=96) == cap.CAP_E_UNSUPPORTED
     assert _gdn_status(dv=24) == cap.CAP_E_UNSUPPORTED
-    assert _gdn_status(workspace_bytes=25088 - 16) == cap.CAP_E_SIZE
+    assert _gdn_status(workspace_bytes=12800 - 16) == cap.CAP_E_SIZE
     assert _gdn_status(beta=20484) == cap.CAP_E_ALIGN
     assert _gdn_status(workspace=(1 << 31) + 8) == cap.CAP_E_ALIGN
     # the workspace overlapping an input, an output overlapping the workspace

@@ -173,7 +173,7 @@ def test_gdn_workspace_is_caller_owned(orc):
     inp = gdn_case(29, T, H, dk, dv)
     d = _dev(inp)
     need = cap.gdn_workspace_bytes(T, H)
-    assert need == 3 * H * 25088
+    assert need == 3 * H * 12800
     ws = torch.full((need,), 0x7F, dtype=torch.uint8, device="cuda")  # NaN patterns
     o = torch.empty((T, H, dv), dtype=torch.float32, device="cuda")
     fs = torch.empty((H, dk, dv), dtype=torch.float32, device="cuda")

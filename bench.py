@@ -25,7 +25,9 @@ environments, a gallery of 8 capsules, 1000 batched gather-restores) under
 
 The JSON line's `value` is the capsule restore bandwidth (GB/s, bytes read +
 written); the scan and TTFT figures ride along as extra keys.  `roofline`
-covers the dominant kernel (the scan, phase 1) and `roofline_copy` the restore.
+covers the dominant kernel (the scan, phase 1); `roofline_copy`,
+`roofline_snapshot` and `roofline_fork` the capsule copies, `gdn` and
+`gather` carry their own.
 Inputs are synthetic (synth module, fixed seeds); 4 distinct layers of q/k/v/g
 are generated on the host and copied into the 36 layers' own device buffers.
 """
@@ -53,6 +55,12 @@ MEASURED_TRAFFIC = {
     "restore": {"src": "paper_2606_20537_amd/csrc/capsule_copy.hip",
                 "sha256": "7c114eda4a9bfbb8004abca49d610710b02b7f73425ed97266d767f35e4ffc66",
                 "bytes": 1763895780},
+    "snapshot": {"src": "paper_2606_20537_amd/csrc/capsule_copy.hip",
+                 "sha256": "7c114eda4a9bfbb8004abca49d610710b02b7f73425ed97266d767f35e4ffc66",
+                 "bytes": 1763952498},
+    "fork4": {"src": "paper_2606_20537_amd/csrc/capsule_copy.hip",
+              "sha256": "7c114eda4a9bfbb8004abca49d610710b02b7f73425ed97266d767f35e4ffc66",
+              "bytes": 4410198017},
     "gather": {"src": "paper_2606_20537_amd/csrc/capsule_copy.hip",
                "sha256": "7c114eda4a9bfbb8004abca49d610710b02b7f73425ed97266d767f35e4ffc66",
                "bytes": 1063125363},
@@ -566,6 +574,18 @@ def main():
                           "achieved": round(restore_gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                           "frac": round(restore_gbs / HBM_PEAK_GBS, 4), "traffic": measured_traffic("restore"),
                           "algorithmic_bytes_per_launch": 2 * cap_bytes, "avg_launch_ms": round(ms["restore"], 5)},
+        "roofline_snapshot": {"kernel": "capsule_copy_kernel (snapshot)", "bound": "hbm",
+                              "achieved": round(2 * cap_bytes / (ms["snapshot"] * 1e-3) / 1e9, 2),
+                              "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                              "frac": round(2 * cap_bytes / (ms["snapshot"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                              "traffic": measured_traffic("snapshot"),
+                              "algorithmic_bytes_per_launch": 2 * cap_bytes, "avg_launch_ms": round(ms["snapshot"], 5)},
+        "roofline_fork": {"kernel": "capsule_copy_kernel (fork x%d)" % n_fork, "bound": "hbm",
+                          "achieved": round((1 + n_fork) * cap_bytes / (ms["fork"] * 1e-3) / 1e9, 2),
+                          "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                          "frac": round((1 + n_fork) * cap_bytes / (ms["fork"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                          "traffic": measured_traffic("fork4") if n_fork == 4 else None,
+                          "algorithmic_bytes_per_launch": (1 + n_fork) * cap_bytes, "avg_launch_ms": round(ms["fork"], 5)},
         "roofline_scan_final_only": {"bound": "hbm", "algorithmic_bytes_per_launch": scan_b_final,
                                      "achieved": round(scan_b_final / (ms["scan_final"] / n_lin * 1e-3) / 1e9, 2),
                                      "unit": "GB/s"},

@@ -50,8 +50,8 @@ LINK_PEAK_GBS = 64.0         # host link, PCIe 5.0 x16, one direction
 # unchanged.  Summary and commands: profiles/hybrid48_hbm_traffic.md.
 MEASURED_TRAFFIC = {
     "scan_cs": {"src": "paper_2606_20537_amd/csrc/linattn_scan.hip",
-                "sha256": "4e94cc48d418f2c361515f87ec31077fae0d35ae3c6e524a8ddc6fce31975868",
-                "bytes": 1227929385},
+                "sha256": "2bd2973a3e90e694c1690fc80bdc814a1112ea5bbe76fe2b30d4c3ea104cada8",
+                "bytes": 1227768690},
     "restore": {"src": "paper_2606_20537_amd/csrc/capsule_copy.hip",
                 "sha256": "7c114eda4a9bfbb8004abca49d610710b02b7f73425ed97266d767f35e4ffc66",
                 "bytes": 1763895780},

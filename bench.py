@@ -50,8 +50,8 @@ LINK_PEAK_GBS = 64.0         # host link, PCIe 5.0 x16, one direction
 # unchanged.  Summary and commands: profiles/hybrid48_hbm_traffic.md.
 MEASURED_TRAFFIC = {
     "scan_cs": {"src": "paper_2606_20537_amd/csrc/linattn_scan.hip",
-                "sha256": "2bd2973a3e90e694c1690fc80bdc814a1112ea5bbe76fe2b30d4c3ea104cada8",
-                "bytes": 1227768690},
+                "sha256": "162440648dff978016a93b9f6e267fc00fad03f344b672ae799c6c1d6802d591",
+                "bytes": 1227813135},
     "restore": {"src": "paper_2606_20537_amd/csrc/capsule_copy.hip",
                 "sha256": "7c114eda4a9bfbb8004abca49d610710b02b7f73425ed97266d767f35e4ffc66",
                 "bytes": 1763895780},

@@ -671,9 +671,11 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
     x.v_row = (int64_t)x.H * x.dv * ES;
     x.o_row = (int64_t)x.H * x.dv * 4;
 
-    // The V-and-gate wave (wave 4) has the longest step of the eight and
-    // arrives last at each barrier; it wins instruction issue on its SIMD.
+    // Issue priority follows the step lengths: the V-and-gate wave (wave 4)
+    // has the longest step of the eight and arrives last at each barrier, the
+    // output waves come next, the other state waves finish first.
     if (wave == 4) __builtin_amdgcn_s_setprio(3);
+    if (wave < 4) __builtin_amdgcn_s_setprio(1);
     switch (wave) {
         case 0: output_role<DK, F32, ONE, 0>(p, sm, x); break;
         case 1: output_role<DK, F32, ONE, 1>(p, sm, x); break;

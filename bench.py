@@ -285,8 +285,8 @@ def main():
         (one append launch), then the 36 one-token recurrent updates."""
         cap.cap_set_append(live, tok_src, 1, stream=strm)
         for L in layers:
-            cap.linattn_chunked_prefill(L["q1"], L["k1"], L["v1"], L["g1"], L["o1"], state_in=L["state"],
-                                        final_state=L["state"], stream=strm)
+            cap.linattn_decode_step(L["q1"], L["k1"], L["v1"], L["g1"], L["o1"], state_in=L["state"],
+                                    final_state=L["state"], stream=strm)
 
     def step(record):
         ev = {k: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for k in phases}

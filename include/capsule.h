@@ -32,8 +32,17 @@
  *     asynchronous and stream-ordered; buffers and arenas must stay alive
  *     until the stream has passed the call.
  *   - Every function returns CAP_OK (0) or a negative CAP_E_* status.  All
- *     argument checks run on the host first: on any error nothing has been
- *     enqueued and no device byte has been written.
+ *     argument checks run on the host first, and a call that needs several
+ *     launches builds and checks every launch's table before it enqueues the
+ *     first: on any error other than CAP_E_HIP nothing has been enqueued and
+ *     no device byte has been written.  CAP_E_HIP reports a launch the HIP
+ *     runtime refused; in a multi-launch call (a fork into many sets, a
+ *     gather of more than 64 environments, an append to more than 128
+ *     buffers) the launches before it stay enqueued.
+ *   - The library reads launch status from the launch calls themselves and
+ *     never clears an error the caller left pending (the runtime's "last
+ *     error"); it clears only the error its own pointer-attribute query
+ *     raises for an unknown arena, and only when none was pending before.
  *   - Not thread-safe for concurrent calls on the same set or capsule.
  */
 #ifndef CAPSULE_H
@@ -61,6 +70,7 @@ extern "C" {
 #define CAP_E_STATE        (-6)  /* set position is not the aligned boundary, or the
                                      capsule is not device-resident                   */
 #define CAP_E_HIP          (-7)  /* HIP runtime error (no device, allocation, launch)  */
+#define CAP_E_NOMEM        (-8)  /* host memory allocation failed                     */
 
 /* Static message for a status code (never NULL). */
 CAP_API const char* cap_status_string(int status);
@@ -238,10 +248,9 @@ CAP_API uint64_t capsule_digest_tokens(const int32_t* ids, uint64_t n);
  *     S_{j+1} = exp(G_last) S_j + sum_m exp(G_last - G_m) k_m^T v_m
  * The arithmetic of a chunk depends only on (S_j, that chunk's inputs): a
  * call started at a chunk-aligned position from a restored state reproduces,
- * bit for bit, what one longer call computes for the same tokens.  A call of
- * exactly one bf16 token (a decode step) takes a shorter path whose state is
- * bit-identical to the chunked one's and whose o may differ from it in fp32
- * rounding only.
+ * bit for bit, what one longer call computes for the same tokens.  This
+ * holds for every T >= 1, so a remainder of one token re-prefilled after a
+ * restore equals the cold prefill's last chunk bit for bit.
  *
  * Layouts (all contiguous, device, caller-owned):
  *   q, k : [T, H, dk]  in_dtype (bf16 or f32)      v : [T, H, dv] in_dtype
@@ -279,6 +288,19 @@ typedef struct linattn_args {
 
 CAP_API int linattn_chunked_prefill(const linattn_args* args, void* stream);
 
+/* One decode step (§3 Algorithm 1: after restore the session appends and
+ * decodes token by token): the recurrence above for exactly one token
+ * (args->T == 1, CAP_E_UNSUPPORTED otherwise), with the same arguments,
+ * layouts and checks as linattn_chunked_prefill.  bf16 tokens take a short
+ * vector-ALU path: its state is bit-identical to the chunked fold of a
+ * one-token chunk (the product of two bf16 values is exact in fp32 and the
+ * fold is one fma with exp(g)); its o takes another summation order, so it
+ * may differ from a one-token prefill's o in fp32 rounding.  fp32 inputs
+ * take the chunked path.  Decode steps are reproducible among themselves:
+ * a session restored at P' and decoded equals a cold session decoded from
+ * the same state, bit for bit. */
+CAP_API int linattn_decode_step(const linattn_args* args, void* stream);
+
 /* -------------------------------------- chunked gated delta-rule prefill -- */
 /* Gated DeltaNet state of the paper's hybrid model (§2 "hybrid recurrent
  * state", §7 model description; the paper does not write the recurrence,
@@ -294,10 +316,8 @@ CAP_API int linattn_chunked_prefill(const linattn_args* args, void* stream);
  * S_new = gamma_last S + sum_m exp(G_last - G_m) k_m^T u_m.  As for the
  * linear-attention scan, a chunk's arithmetic depends only on (S, that
  * chunk's inputs): restore at an aligned position then continue equals one
- * longer call bit for bit.  A call of exactly one token (a decode step) is
- * one launch on a shorter path (with A = 0 and (I + A)^-1 = I) whose state
- * and o agree with the chunked path's to fp32 rounding; it does not touch
- * the workspace.
+ * longer call bit for bit, for every T >= 1 (a one-token call takes the
+ * chunked path too).
  *
  * Layouts (contiguous, device, caller-owned):
  *   q, k : [T, H, dk] bf16     v : [T, H, dv] bf16
@@ -341,6 +361,15 @@ typedef struct gdn_args {
 CAP_API uint64_t gdn_workspace_bytes(int64_t T, int32_t H, int32_t chunk);
 
 CAP_API int gdn_chunked_prefill(const gdn_args* args, void* stream);
+
+/* One decode step of the delta rule: exactly one token (args->T == 1,
+ * CAP_E_UNSUPPORTED otherwise) in one launch on a short vector-ALU path
+ * (with one token A = 0 and (I + A)^-1 = I: u = beta (v - gamma k S),
+ * S' = gamma S + k^T u, o = scale (gamma q S + (q.k) u)).  Same arguments
+ * and checks as gdn_chunked_prefill except that the workspace is not used
+ * (it may be NULL).  State and o agree with a one-token prefill's to fp32
+ * rounding; decode steps are reproducible among themselves. */
+CAP_API int gdn_decode_step(const gdn_args* args, void* stream);
 
 /* ---------------------------------------------------------- FP8 KV ------ */
 /* §3 "Definition": the KV region may be held in FP8, which roughly halves

@@ -6,11 +6,12 @@ csrc/).  This package holds its build script and a ctypes binding whose
 functions carry the C entry points' names.
 """
 from ._native import (  # noqa: F401
-    CAP_DTYPE_BF16, CAP_DTYPE_F32, CAP_E_ALIGN, CAP_E_DIGEST, CAP_E_HIP, CAP_E_INVAL, CAP_E_SIZE,
+    CAP_DTYPE_BF16, CAP_DTYPE_F32, CAP_E_ALIGN, CAP_E_DIGEST, CAP_E_HIP, CAP_E_INVAL, CAP_E_NOMEM, CAP_E_SIZE,
     CAP_E_STATE, CAP_E_UNSUPPORTED, CAP_KIND_FIXED, CAP_KIND_POSITIONAL, CAP_MAX_BUFFERS, CAP_MAX_FORK,
     CAP_MAX_GALLERY, CAP_OK, CAP_TIER_DEVICE, CAP_TIER_HOST, SIGNATURES, CapSet, Capsule, CapsuleError, cap_align_boundary, cap_set_append, cap_set_create,
     cap_set_destroy, cap_set_get_position, cap_set_set_position, cap_status_string, capsule_bytes,
     capsule_digest_tokens, capsule_fork, capsule_gather_restore, capsule_info, capsule_layout_bytes,
     capsule_move, capsule_release, capsule_restore, capsule_snapshot, capsule_tier, gdn_chunked_prefill,
-    gdn_workspace_bytes, kv_fp8_dequantize, kv_fp8_quantize, linattn_chunked_prefill, load,
+    gdn_decode_step, gdn_workspace_bytes, kv_fp8_dequantize, kv_fp8_quantize, linattn_chunked_prefill,
+    linattn_decode_step, load,
 )

@@ -20,6 +20,7 @@ CAP_E_UNSUPPORTED = -4
 CAP_E_ALIGN = -5
 CAP_E_STATE = -6
 CAP_E_HIP = -7
+CAP_E_NOMEM = -8
 
 CAP_KIND_POSITIONAL = 0
 CAP_KIND_FIXED = 1
@@ -90,8 +91,10 @@ SIGNATURES = [
     ("capsule_release", ct.c_int, [_vp]),
     ("capsule_digest_tokens", _u64, [ct.POINTER(_i32), _u64]),
     ("linattn_chunked_prefill", ct.c_int, [ct.POINTER(linattn_args), _vp]),
+    ("linattn_decode_step", ct.c_int, [ct.POINTER(linattn_args), _vp]),
     ("gdn_workspace_bytes", _u64, [ct.c_int64, _i32, _i32]),
     ("gdn_chunked_prefill", ct.c_int, [ct.POINTER(gdn_args), _vp]),
+    ("gdn_decode_step", ct.c_int, [ct.POINTER(gdn_args), _vp]),
 ]
 
 _lib = None
@@ -318,19 +321,31 @@ def capsule_digest_tokens(ids):
     return int(load().capsule_digest_tokens(a.ctypes.data_as(ct.POINTER(_i32)), a.size))
 
 
-def linattn_chunked_prefill(q, k, v, g, o, *, state_in=None, chunk_states=None, final_state=None,
-                            T=None, H=None, dk=None, dv=None, chunk=64, in_dtype=None, scale=1.0,
-                            stream=None):
-    """Marshal tensors (or addresses with explicit sizes) into linattn_args."""
+def _linattn_args(q, k, v, g, o, state_in, chunk_states, final_state, T, H, dk, dv, chunk, in_dtype, scale):
     if T is None:
         T, H, dk = q.shape
         dv = v.shape[2]
     if in_dtype is None:
         import torch
         in_dtype = CAP_DTYPE_F32 if q.dtype == torch.float32 else CAP_DTYPE_BF16
-    a = linattn_args(_addr(q), _addr(k), _addr(v), _addr(g), _addr(state_in), _addr(o), _addr(chunk_states),
-                     _addr(final_state), int(T), int(H), int(dk), int(dv), int(chunk), int(in_dtype), float(scale))
+    return linattn_args(_addr(q), _addr(k), _addr(v), _addr(g), _addr(state_in), _addr(o), _addr(chunk_states),
+                        _addr(final_state), int(T), int(H), int(dk), int(dv), int(chunk), int(in_dtype),
+                        float(scale))
+
+
+def linattn_chunked_prefill(q, k, v, g, o, *, state_in=None, chunk_states=None, final_state=None,
+                            T=None, H=None, dk=None, dv=None, chunk=64, in_dtype=None, scale=1.0,
+                            stream=None):
+    """Marshal tensors (or addresses with explicit sizes) into linattn_args."""
+    a = _linattn_args(q, k, v, g, o, state_in, chunk_states, final_state, T, H, dk, dv, chunk, in_dtype, scale)
     return _check("linattn_chunked_prefill", load().linattn_chunked_prefill(ct.byref(a), _stream(stream)))
+
+
+def linattn_decode_step(q, k, v, g, o, *, state_in=None, final_state=None, T=None, H=None, dk=None, dv=None,
+                        chunk=64, in_dtype=None, scale=1.0, stream=None):
+    """One decode token (T == 1): the same arguments as linattn_chunked_prefill."""
+    a = _linattn_args(q, k, v, g, o, state_in, None, final_state, T, H, dk, dv, chunk, in_dtype, scale)
+    return _check("linattn_decode_step", load().linattn_decode_step(ct.byref(a), _stream(stream)))
 
 
 def gdn_workspace_bytes(T, H, chunk=64):
@@ -359,6 +374,18 @@ def gdn_chunked_prefill(q, k, v, g, beta, o, *, state_in=None, chunk_states=None
                  _addr(chunk_states), _addr(final_state), _addr(workspace), int(workspace_bytes), int(T), int(H),
                  int(dk), int(dv), int(chunk), int(in_dtype), float(scale))
     return _check("gdn_chunked_prefill", load().gdn_chunked_prefill(ct.byref(a), _stream(stream)))
+
+
+def gdn_decode_step(q, k, v, g, beta, o, *, state_in=None, final_state=None, T=None, H=None, dk=None, dv=None,
+                    chunk=64, in_dtype=CAP_DTYPE_BF16, scale=1.0, stream=None):
+    """One decode token (T == 1) of the delta rule; no workspace."""
+    if T is None:
+        T, H, dk = q.shape
+        dv = v.shape[2]
+    a = gdn_args(_addr(q), _addr(k), _addr(v), _addr(g), _addr(beta), _addr(state_in), _addr(o), 0,
+                 _addr(final_state), 0, 0, int(T), int(H), int(dk), int(dv), int(chunk), int(in_dtype),
+                 float(scale))
+    return _check("gdn_decode_step", load().gdn_decode_step(ct.byref(a), _stream(stream)))
 
 
 def _fp8_segs(segs):

@@ -80,8 +80,7 @@ __global__ __launch_bounds__(kThreads) void append_kernel(const AppendParams p) 
 hipError_t launch_append(const AppendParams& p, hipStream_t stream) {
     const uint32_t blocks = p.first_block[p.n_seg];
     if (blocks == 0) return hipSuccess;
-    hipLaunchKernelGGL(append_kernel, dim3(blocks), dim3(kThreads), 0, stream, p);
-    return hipGetLastError();
+    return launch_kernel(reinterpret_cast<const void*>(&append_kernel), dim3(blocks), dim3(kThreads), p, stream);
 }
 
 }  // namespace cap

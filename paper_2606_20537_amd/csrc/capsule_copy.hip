@@ -186,22 +186,43 @@ __global__ __launch_bounds__(kThreads) void capsule_copy_kernel(const CopyParams
 
 }  // namespace
 
+namespace {
+
+// tile shape of each verb (see launch_copy)
+struct Shape {
+    uint64_t threads, unroll, ptr;
+};
+
+Shape shape_of(const CopyParams& p) {
+    if (p.n_dst > 1) return {512, 1, (uint64_t)kMaxPtrLds};
+    return {256, 4, (uint64_t)kMaxSeg};
+}
+
+uint64_t tiles_of(const CopyParams& p) {
+    const Shape s = shape_of(p);
+    // one block per tile; every buffer adds at most one partial tile
+    return (p.nvec / (s.threads * s.unroll) + p.n_seg) * p.n_rep;
+}
+
 template <int kThreads, int kUnroll, bool NT_LD, bool NT_ST, int kPtr>
 hipError_t launch_t(const CopyParams& p, hipStream_t stream) {
-    constexpr uint64_t kTileVec = (uint64_t)kThreads * kUnroll;
-    if (p.n_seg * p.n_dst > (uint32_t)kPtr) return hipErrorInvalidValue;
-    // one block per tile; every buffer adds at most one partial tile
-    const uint64_t tiles = (p.nvec / kTileVec + p.n_seg) * p.n_rep;
-    if (tiles > 0x7fffffffull) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((capsule_copy_kernel<kThreads, kUnroll, NT_LD, NT_ST, kPtr>), dim3((unsigned)tiles),
-                       dim3(kThreads), 0, stream, p);
-    return hipGetLastError();
+    return launch_kernel(reinterpret_cast<const void*>(&capsule_copy_kernel<kThreads, kUnroll, NT_LD, NT_ST, kPtr>),
+                         dim3((unsigned)tiles_of(p)), dim3(kThreads), p, stream);
+}
+
+}  // namespace
+
+bool copy_params_ok(const CopyParams& p) {
+    if (p.nvec == 0 || p.n_rep == 0) return true;
+    if (p.n_seg > (uint32_t)kMaxSeg || (uint64_t)p.n_seg * p.n_dst > (uint64_t)kMaxPtrLds) return false;
+    if ((uint64_t)p.n_seg * p.n_dst > shape_of(p).ptr) return false;
+    return tiles_of(p) <= 0x7fffffffull;
 }
 
 hipError_t launch_copy(const CopyParams& p, int num_cus, hipStream_t stream) {
     (void)num_cus;
     if (p.nvec == 0 || p.n_rep == 0) return hipSuccess;
-    if (p.n_seg > (uint32_t)kMaxSeg || p.n_seg * p.n_dst > (uint32_t)kMaxPtrLds) return hipErrorInvalidValue;
+    if (!copy_params_ok(p)) return hipErrorInvalidValue;
     // Tile shapes chosen by measurement on MI355X:
     //  * snapshot / restore (882 MB capsule): 16 KiB tiles, loads and stores
     //    streamed past the caches;

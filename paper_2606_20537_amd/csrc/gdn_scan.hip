@@ -666,14 +666,14 @@ template <int DK>
 hipError_t launch_t(const GdnParams& p, hipStream_t stream) {
     const int64_t n = (p.T + CH - 1) / CH;
     if (n > 0) {
-        hipLaunchKernelGGL((gdn_prepare_kernel<DK>), dim3((unsigned)(n * p.H)), dim3(64), 0, stream, p);
-        const hipError_t e = hipGetLastError();
+        const hipError_t e = launch_kernel(reinterpret_cast<const void*>(&gdn_prepare_kernel<DK>),
+                                           dim3((unsigned)(n * p.H)), dim3(64), p, stream);
         if (e != hipSuccess) return e;
     }
     const dim3 grid((unsigned)(p.H * (p.dv / DVS)));
-    if (p.T <= CH) hipLaunchKernelGGL((gdn_scan_kernel<DK, true>), grid, dim3(NT), 0, stream, p);
-    else hipLaunchKernelGGL((gdn_scan_kernel<DK, false>), grid, dim3(NT), 0, stream, p);
-    return hipGetLastError();
+    const void* fn = p.T <= CH ? reinterpret_cast<const void*>(&gdn_scan_kernel<DK, true>)
+                               : reinterpret_cast<const void*>(&gdn_scan_kernel<DK, false>);
+    return launch_kernel(fn, grid, dim3(NT), p, stream);
 }
 
 }  // namespace

@@ -114,10 +114,9 @@ __global__ __launch_bounds__(2 * DK) void gdn_step_kernel(const GdnParams p) {
 hipError_t launch_gdn_step(const GdnParams& p, hipStream_t stream) {
     const unsigned grid = (unsigned)(p.H * (p.dv / DVS));
     if (p.T != 1) return hipErrorInvalidValue;
-    if (p.dk == 128) hipLaunchKernelGGL((gdn_step_kernel<128>), dim3(grid), dim3(256), 0, stream, p);
-    else if (p.dk == 64) hipLaunchKernelGGL((gdn_step_kernel<64>), dim3(grid), dim3(128), 0, stream, p);
-    else return hipErrorInvalidValue;
-    return hipGetLastError();
+    if (p.dk == 128) return launch_kernel(reinterpret_cast<const void*>(&gdn_step_kernel<128>), dim3(grid), dim3(256), p, stream);
+    if (p.dk == 64) return launch_kernel(reinterpret_cast<const void*>(&gdn_step_kernel<64>), dim3(grid), dim3(128), p, stream);
+    return hipErrorInvalidValue;
 }
 
 }  // namespace cap

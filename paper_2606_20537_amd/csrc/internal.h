@@ -7,7 +7,19 @@
 #include <hip/hip_runtime_api.h>
 #include <stdint.h>
 
+#include "capsule.h"
+
 namespace cap {
+
+// Launch a kernel whose one argument is a parameter struct passed by value
+// and return that launch's own status.  The library never calls
+// hipGetLastError, so an error the caller left pending is neither read nor
+// cleared by a launch.
+template <class P>
+inline hipError_t launch_kernel(const void* fn, dim3 grid, dim3 block, const P& p, hipStream_t stream) {
+    void* args[] = {const_cast<P*>(&p)};
+    return hipLaunchKernel(fn, grid, block, args, 0, stream);
+}
 
 // One entry of a live set's static device segment table.  For buffer i of a
 // set, with the boundary P' chosen per call:
@@ -47,6 +59,9 @@ struct CopyParams {
     int32_t         mode;
 };
 
+// Whether launch_copy accepts p (grid and LDS-table limits); a multi-launch
+// call checks every launch with it before enqueueing the first one.
+bool copy_params_ok(const CopyParams& p);
 // Launch the descriptor-driven copy.  Returns hipSuccess or the launch error.
 hipError_t launch_copy(const CopyParams& p, int num_cus, hipStream_t stream);
 
@@ -65,6 +80,10 @@ struct ScanParams {
     int32_t      in_f32;   // 1: q/k/v are fp32, 0: bf16
     float        scale;
 };
+
+// Host checks of a linattn_args (status codes as documented in capsule.h);
+// on CAP_OK *out holds the launch parameters.
+int validate_linattn(const linattn_args* a, ScanParams* out);
 
 hipError_t launch_linattn_scan(const ScanParams& p, hipStream_t stream);
 // T == 1, bf16 inputs (a decode step); same contract as launch_linattn_scan
@@ -95,6 +114,11 @@ struct GdnParams {
     int32_t      H, dk, dv;
     float        scale;
 };
+
+// Host checks of a gdn_args; need_ws: the call reads args->workspace (a
+// decode step does not).  On CAP_OK *out holds the launch parameters (ws =
+// the caller's workspace, or NULL when need_ws is false).
+int validate_gdn(const gdn_args* a, bool need_ws, GdnParams* out);
 
 hipError_t launch_gdn(const GdnParams& p, hipStream_t stream);
 // T == 1 (a decode step): one launch, no workspace use

@@ -145,9 +145,9 @@ __global__ __launch_bounds__(256) void fp8_kernel(const Fp8Params p) {
 hipError_t launch_fp8(const Fp8Params& p, hipStream_t stream) {
     const uint32_t blocks = p.first_block[p.n_seg];
     if (blocks == 0) return hipSuccess;
-    if (p.quantize) hipLaunchKernelGGL((fp8_kernel<true>), dim3(blocks), dim3(256), 0, stream, p);
-    else hipLaunchKernelGGL((fp8_kernel<false>), dim3(blocks), dim3(256), 0, stream, p);
-    return hipGetLastError();
+    const void* fn = p.quantize ? reinterpret_cast<const void*>(&fp8_kernel<true>)
+                                : reinterpret_cast<const void*>(&fp8_kernel<false>);
+    return launch_kernel(fn, dim3(blocks), dim3(256), p, stream);
 }
 
 }  // namespace cap

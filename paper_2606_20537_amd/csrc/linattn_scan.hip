@@ -689,9 +689,9 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
 template <int DK, bool F32>
 hipError_t launch_t(const ScanParams& p, hipStream_t stream) {
     const unsigned grid = (unsigned)(p.H * (p.dv / DVS));
-    if (p.T <= CH) hipLaunchKernelGGL((linattn_scan_kernel<DK, F32, true>), dim3(grid), dim3(NT), 0, stream, p);
-    else hipLaunchKernelGGL((linattn_scan_kernel<DK, F32, false>), dim3(grid), dim3(NT), 0, stream, p);
-    return hipGetLastError();
+    const void* fn = p.T <= CH ? reinterpret_cast<const void*>(&linattn_scan_kernel<DK, F32, true>)
+                               : reinterpret_cast<const void*>(&linattn_scan_kernel<DK, F32, false>);
+    return launch_kernel(fn, dim3(grid), dim3(NT), p, stream);
 }
 
 }  // namespace

@@ -104,10 +104,11 @@ __global__ __launch_bounds__(2 * DK) void linattn_step_kernel(const ScanParams p
 hipError_t launch_linattn_step(const ScanParams& p, hipStream_t stream) {
     const unsigned grid = (unsigned)(p.H * (p.dv / DVS));
     if (p.in_f32 || p.T != 1) return hipErrorInvalidValue;
-    if (p.dk == 128) hipLaunchKernelGGL((linattn_step_kernel<128>), dim3(grid), dim3(256), 0, stream, p);
-    else if (p.dk == 64) hipLaunchKernelGGL((linattn_step_kernel<64>), dim3(grid), dim3(128), 0, stream, p);
-    else return hipErrorInvalidValue;
-    return hipGetLastError();
+    if (p.dk == 128)
+        return launch_kernel(reinterpret_cast<const void*>(&linattn_step_kernel<128>), dim3(grid), dim3(256), p, stream);
+    if (p.dk == 64)
+        return launch_kernel(reinterpret_cast<const void*>(&linattn_step_kernel<64>), dim3(grid), dim3(128), p, stream);
+    return hipErrorInvalidValue;
 }
 
 }  // namespace cap

@@ -2,6 +2,9 @@
 
 Inputs come from ``synth`` and expected values from ``oracle``; nothing here
 computes any part of the method."""
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 
 import synth
@@ -39,6 +42,37 @@ def rel_err(x, y):
     den = float(np.max(np.abs(y)))
     num = float(np.max(np.abs(x - y)))
     return num / den if den > 0 else num
+
+
+def elem_err(x, y, floor=1e-3):
+    """max_i |x_i - y_i| / max(|y_i|, floor * max|y|): the elementwise
+    relative error with a magnitude floor (elements far below the tensor's
+    scale are measured against the floor)."""
+    x = np.asarray(x, np.float64)
+    y = np.asarray(y, np.float64)
+    if x.size == 0:
+        return 0.0
+    fl = floor * float(np.max(np.abs(y)))
+    den = np.maximum(np.abs(y), fl)
+    if fl == 0:
+        den = np.where(den == 0, 1.0, den)
+    return float(np.max(np.abs(x - y) / den))
+
+
+def oracle_threads():
+    """Worker threads for head-parallel oracle runs (the C oracle releases
+    the GIL inside each call); at most 16, the CPU share of one GPU."""
+    return max(1, min(16, len(os.sched_getaffinity(0))))
+
+
+def by_head(fn, arrays, heads):
+    """Run an oracle function on each head h of ``heads`` separately (arrays
+    sliced [:, h:h+1] along the head axis, made contiguous) in worker
+    threads; returns the list of per-head results, in order."""
+    def one(h):
+        return fn(*[np.ascontiguousarray(a[:, h:h + 1]) for a in arrays])
+    with ThreadPoolExecutor(oracle_threads()) as ex:
+        return list(ex.map(one, heads))
 
 
 def scan_case(seed, T, H, dk, dv, dtype="bf16", gate_mu=3.0, gate_sigma=0.5):

@@ -81,30 +81,39 @@ class HybridStack:
         cap.cap_set_append(self.set, srcs, t1 - t0)
 
     # --- the hot path -----------------------------------------------------
-    def prefill(self, t0, t1):
-        """Run tokens [t0, t1) through every linear layer (one call each)."""
+    def prefill(self, t0, t1, decode=False):
+        """Run tokens [t0, t1) through every linear layer (one call each):
+        the chunked prefill, or with decode=True (one token) the decode step."""
         assert t0 == self.pos, (t0, self.pos)
+        assert not decode or t1 == t0 + 1
         w = self.w
         T = t1 - t0
         for l in range(w.n_linear):
             d = self.inp["lin"][l]
             if self.mixer == "gdn":
-                cap.gdn_chunked_prefill(d["q"][t0:t1], d["k"][t0:t1], d["v"][t0:t1], d["g"][t0:t1],
+                if decode:
+                    cap.gdn_decode_step(d["q"][t0:t1], d["k"][t0:t1], d["v"][t0:t1], d["g"][t0:t1],
                                         d["beta"][t0:t1], self.o[l][t0:t1], state_in=self.state[l],
-                                        final_state=self.state[l], workspace=self.ws,
-                                        T=T, H=w.heads, dk=w.dk, dv=w.dv, chunk=w.chunk)
+                                        final_state=self.state[l], T=T, H=w.heads, dk=w.dk, dv=w.dv, chunk=w.chunk)
+                else:
+                    cap.gdn_chunked_prefill(d["q"][t0:t1], d["k"][t0:t1], d["v"][t0:t1], d["g"][t0:t1],
+                                            d["beta"][t0:t1], self.o[l][t0:t1], state_in=self.state[l],
+                                            final_state=self.state[l], workspace=self.ws,
+                                            T=T, H=w.heads, dk=w.dk, dv=w.dv, chunk=w.chunk)
                 continue
-            cap.linattn_chunked_prefill(d["q"][t0:t1], d["k"][t0:t1], d["v"][t0:t1], d["g"][t0:t1],
-                                        self.o[l][t0:t1], state_in=self.state[l], final_state=self.state[l],
-                                        T=T, H=w.heads, dk=w.dk, dv=w.dv, chunk=w.chunk,
-                                        in_dtype=cap.CAP_DTYPE_F32 if w.in_dtype == "f32" else cap.CAP_DTYPE_BF16)
+            fn = cap.linattn_decode_step if decode else cap.linattn_chunked_prefill
+            fn(d["q"][t0:t1], d["k"][t0:t1], d["v"][t0:t1], d["g"][t0:t1],
+               self.o[l][t0:t1], state_in=self.state[l], final_state=self.state[l],
+               T=T, H=w.heads, dk=w.dk, dv=w.dv, chunk=w.chunk,
+               in_dtype=cap.CAP_DTYPE_F32 if w.in_dtype == "f32" else cap.CAP_DTYPE_BF16)
         cap.cap_set_set_position(self.set, t0)
         self._append_rows(t0, t1)
         self.pos = t1
 
     def decode(self, n):
+        """n decode steps (one token each, the decode entry points)."""
         for _ in range(n):
-            self.prefill(self.pos, self.pos + 1)
+            self.prefill(self.pos, self.pos + 1, decode=True)
 
     def snapshot(self, P, digest=0):
         nbytes = cap.capsule_bytes(self.set, P)

@@ -32,7 +32,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_status_strings():
-    for code in (0, -1, -2, -3, -4, -5, -6, -7):
+    for code in (0, -1, -2, -3, -4, -5, -6, -7, -8):
         assert cap.cap_status_string(code) not in ("", "unknown status")
     assert cap.cap_status_string(-99) == "unknown status"
 
@@ -118,6 +118,8 @@ def test_null_handles():
     assert L.capsule_fork(None, None, 0, 0, None) == cap.CAP_E_INVAL
     assert L.capsule_gather_restore(None, 0, None, None, 0, None) == cap.CAP_E_INVAL
     assert L.linattn_chunked_prefill(None, None) == cap.CAP_E_INVAL
+    assert L.linattn_decode_step(None, None) == cap.CAP_E_INVAL
+    assert L.gdn_decode_step(None, None) == cap.CAP_E_INVAL
     h = ct.c_void_p(1)
     assert L.capsule_move(None, None, 0, None, ct.byref(h)) == cap.CAP_E_INVAL
     assert h.value is None
@@ -159,6 +161,74 @@ def test_scan_argument_checks():
     # more heads than 32-bit offsets inside one state of all heads can address
     assert _scan_status(H=32768, dk=128, dv=128) == cap.CAP_E_UNSUPPORTED
     assert _scan_status(H=32767, dk=128, dv=128, T=0, q=0, k=0, v=0, g=0, o=0) == cap.CAP_OK
+
+
+def test_decode_step_argument_checks():
+    """The decode step runs the prefill's checks, then requires T == 1."""
+    L = N.load()
+    for T in (0, 2, 64):
+        assert L.linattn_decode_step(ct.byref(_args(T=T)), None) == cap.CAP_E_UNSUPPORTED
+    assert L.linattn_decode_step(ct.byref(_args(T=1, q=0)), None) == cap.CAP_E_INVAL
+    assert L.linattn_decode_step(ct.byref(_args(T=1, dk=96)), None) == cap.CAP_E_UNSUPPORTED
+    assert L.linattn_decode_step(ct.byref(_args(T=1, o=8192 + 64)), None) == cap.CAP_E_INVAL
+    g = dict(q=4096, k=8192, v=12288, g=16384, beta=20480, state_in=0, o=1 << 30, chunk_states=0,
+             final_state=0, workspace=0, workspace_bytes=0, T=2, H=1, dk=64, dv=16, chunk=64,
+             in_dtype=cap.CAP_DTYPE_BF16, scale=1.0)
+    assert L.gdn_decode_step(ct.byref(N.gdn_args(**g)), None) == cap.CAP_E_UNSUPPORTED
+    g.update(T=1, beta=0)
+    assert L.gdn_decode_step(ct.byref(N.gdn_args(**g)), None) == cap.CAP_E_INVAL
+    g.update(beta=20484)
+    assert L.gdn_decode_step(ct.byref(N.gdn_args(**g)), None) == cap.CAP_E_ALIGN
+
+
+OOM_DRIVER = r"""
+#include <cstdio>
+#include <cstdlib>
+#include <new>
+#include "capsule.h"
+// Global operator new of this executable interposes the library's: once
+// g_fail is set, every host allocation fails.
+static bool g_fail = false;
+void* operator new(std::size_t n) {
+    if (g_fail) throw std::bad_alloc();
+    void* p = std::malloc(n ? n : 1);
+    if (!p) throw std::bad_alloc();
+    return p;
+}
+void* operator new(std::size_t n, const std::nothrow_t&) noexcept { return g_fail ? nullptr : std::malloc(n ? n : 1); }
+void operator delete(void* p) noexcept { std::free(p); }
+void operator delete(void* p, std::size_t) noexcept { std::free(p); }
+int main() {
+    cap_buf b[2] = {{"k", (void*)4096, 64, 10, CAP_KIND_POSITIONAL, 0}, {"s", (void*)65536, 256, 1, CAP_KIND_FIXED, 0}};
+    uint64_t bytes = 0;
+    const int ok = capsule_layout_bytes(b, 2, 64, 0, &bytes);
+    g_fail = true;
+    const int oom_layout = capsule_layout_bytes(b, 2, 64, 0, &bytes);
+    cap_set s = (cap_set)1;
+    const int oom_create = cap_set_create(b, 2, 64, 1, &s);
+    g_fail = false;
+    std::printf("%d %d %d %d\n", ok, oom_layout, oom_create, s == nullptr);
+    return 0;
+}
+"""
+
+
+def test_host_allocation_failure_is_nomem(tmp_path):
+    """A host allocation that fails inside an entry point returns CAP_E_NOMEM
+    (no exception crosses the C boundary) and leaves *out cleared; checked
+    with a driver whose operator new fails on demand."""
+    import shutil
+    import subprocess
+    if shutil.which("g++") is None:
+        pytest.skip("g++ not available")
+    libdir = os.path.dirname(N.LIB_PATH)
+    src = tmp_path / "oom.cpp"
+    src.write_text(OOM_DRIVER)
+    exe = tmp_path / "oom"
+    subprocess.run(["g++", "-std=c++17", "-O1", "-I", os.path.join(ROOT, "include"), "-o", str(exe), str(src),
+                    "-L" + libdir, "-lcapsule", "-Wl,-rpath," + libdir, "-Wl,-rpath,/opt/rocm/lib"], check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split()
+    assert out == [str(cap.CAP_OK), str(cap.CAP_E_NOMEM), str(cap.CAP_E_NOMEM), "1"], out
 
 
 def _gdn_status(**kw):

@@ -210,3 +210,89 @@ def test_explicit_release_then_collection_is_safe():
     s2.destroy()                 # no-op
     del s2
     gc.collect()
+
+
+def test_overlapping_destination_sets_are_rejected():
+    """Two live sets over the same device buffers: a gather writing different
+    capsules into them would race, and a fork would write the same bytes
+    twice -- both are CAP_E_INVAL before anything is enqueued."""
+    import torch
+    s_a, bufs = _make_set(21)
+    s_b = cap.cap_set_create(bufs, CHUNK, KEY)          # the same buffers, another handle
+    s_c, _ = _make_set(22)
+    P = 128
+    cap.cap_set_set_position(s_a, P)
+    arena = device_bytes(cap.capsule_bytes(s_a, P), fill=0)
+    c = cap.capsule_snapshot(s_a, P, 5, arena)
+    torch.cuda.synchronize()
+    before = [b[1].clone() for b in bufs]
+    for call in (lambda: cap.capsule_gather_restore([c], [0, 0], [s_b, s_a]),
+                 lambda: cap.capsule_fork(c, [s_c, s_b, s_a], 5)):
+        with pytest.raises(cap.CapsuleError) as ei:
+            call()
+        assert ei.value.status == cap.CAP_E_INVAL
+    torch.cuda.synchronize()
+    for b, x in zip(bufs, before):
+        assert torch.equal(b[1], x)
+    cap.capsule_fork(c, [s_c, s_b], 5)                    # disjoint destinations are fine
+
+
+def test_rejected_arena_keeps_the_callers_pending_error():
+    """An arena the device cannot address is CAP_E_INVAL; the library clears
+    the error its own pointer query raised only when none was pending, so an
+    error the caller left pending stays pending."""
+    import ctypes as ct
+    import torch
+    hip = ct.CDLL("libamdhip64.so")
+    hip.hipGetLastError.restype = ct.c_int
+    hip.hipPeekAtLastError.restype = ct.c_int
+    hip.hipSetDevice.argtypes = [ct.c_int]
+    s, bufs = _make_set(31)
+    P = 64
+    cap.cap_set_set_position(s, P)
+    pageable = np.zeros(cap.capsule_bytes(s, P) + 64, np.uint8)
+    addr = (pageable.ctypes.data + 15) & ~15
+    torch.cuda.synchronize()
+    assert hip.hipGetLastError() == 0
+    # nothing pending: the query's own error is cleared
+    with pytest.raises(cap.CapsuleError) as ei:
+        cap.capsule_snapshot(s, P, 0, addr, arena_bytes=cap.capsule_bytes(s, P))
+    assert ei.value.status == cap.CAP_E_INVAL
+    assert hip.hipPeekAtLastError() == 0
+    # does the runtime keep an error pending across a successful call?
+    dev = ct.c_int(-1)
+    hip.hipGetDevice.argtypes = [ct.POINTER(ct.c_int)]
+    assert hip.hipSetDevice(1 << 20) != 0                  # an invalid device index: a host-side error
+    assert hip.hipGetDevice(ct.byref(dev)) == 0
+    sticky = hip.hipPeekAtLastError() != 0
+    hip.hipGetLastError()
+    if not sticky:
+        print("this runtime clears the stored error on every successful call; nothing can stay pending")
+        return
+    # an error left pending by the caller survives the call
+    assert hip.hipSetDevice(1 << 20) != 0
+    with pytest.raises(cap.CapsuleError):
+        cap.capsule_snapshot(s, P, 0, addr, arena_bytes=cap.capsule_bytes(s, P))
+    assert hip.hipPeekAtLastError() != 0
+    assert hip.hipGetLastError() != 0                      # cleared here, by the caller
+    assert hip.hipGetLastError() == 0
+
+
+def test_append_across_two_launches_matches_oracle(orc):
+    """An append to 200 buffers takes two launches (128 buffers each at most);
+    every row lands where the oracle's append puts it."""
+    import torch
+    layout = [("p%d" % i, 32 * (1 + i % 3), 40, cap.CAP_KIND_POSITIONAL) for i in range(150)]
+    layout += [("w%d" % i, 64, 4, cap.CAP_KIND_FIXED) for i in range(50)]
+    s, bufs = _make_set(41, layout)
+    pos, n = 7, 5
+    cap.cap_set_set_position(s, pos)
+    srcs = [device_bytes(n * rb, seed=4100 + i, name="src%d" % i) for i, (_, rb, _, _) in enumerate(layout)]
+    host = _host(bufs)
+    cap.cap_set_append(s, srcs, n)
+    torch.cuda.synchronize()
+    rb, rt, kd = _lay(bufs)
+    assert orc.append(host, [x.cpu().numpy() for x in srcs], rb, rt, kd, pos, n) == 0
+    for b, want in zip(bufs, host):
+        assert np.array_equal(b[1].cpu().numpy(), want), b[0]
+    assert cap.cap_set_get_position(s) == pos + n

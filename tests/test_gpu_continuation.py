@@ -8,7 +8,7 @@ import pytest
 import torch
 
 import synth
-from gpu_util import PARITY_TOL, rel_err
+from gpu_util import PARITY_TOL, by_head, rel_err
 from harness import HybridStack, make_inputs
 
 pytestmark = pytest.mark.gpu
@@ -81,16 +81,50 @@ def test_hybrid8_capsule_then_decode_steps(orc, inputs_hyb8):
         assert rel_err(cold.state[l].cpu().numpy(), s_ref) <= PARITY_TOL, l
 
 
+ALIGN_T = 8192 + 63 + 32
+ALIGN_PREFIXES = list(range(1024, 8193, 1024))
+
+
 @pytest.fixture(scope="module")
 def inputs_align():
-    return make_inputs(ALIGN, 8192 + 63 + 32, ALIGN.seed)
+    return make_inputs(ALIGN, ALIGN_T, ALIGN.seed)
 
 
-@pytest.mark.parametrize("L", list(range(1024, 8193, 1024)))
+@pytest.fixture(scope="module")
+def oracle_align(orc, inputs_align):
+    """The oracle's chunked form over every token the sweep uses, per layer
+    and head: o for all tokens, and the states entering the chunks at L and
+    L + 64 for every swept L (the sweep's final states lie in those chunks)."""
+    keep = sorted({L // 64 for L in ALIGN_PREFIXES} | {L // 64 + 1 for L in ALIGN_PREFIXES})
+    out = []
+    for l in range(ALIGN.n_linear):
+        h = inputs_align["lin"][l]["host"]
+        arrs = [h[n][:ALIGN_T] for n in ("q", "k", "v", "g")]
+        res = by_head(lambda q, k, v, g: orc.chunked(q, k, v, g, 64), arrs, range(ALIGN.heads))
+        o = np.concatenate([r[0] for r in res], axis=1)
+        cs = {j: np.concatenate([r[1][j] for r in res], axis=0) for j in keep}
+        out.append({"o": o, "cs": cs})
+    return out
+
+
+def oracle_state_at(orc, inputs, ref, l, F):
+    """The oracle's state after token F - 1 of layer l: the chunked form's
+    state entering the chunk of F, advanced token by token by the sequential
+    recurrence."""
+    j = F // 64
+    h = inputs["lin"][l]["host"]
+    sub = [np.ascontiguousarray(h[n][64 * j:F]) for n in ("q", "k", "v", "g")]
+    _, S = orc.sequential(*sub, S0=ref[l]["cs"][j])
+    return S
+
+
+@pytest.mark.parametrize("L", ALIGN_PREFIXES)
 @pytest.mark.parametrize("off", [0, 2, 63])
-def test_alignment_sweep(inputs_align, L, off):
+def test_alignment_sweep(orc, inputs_align, oracle_align, L, off):
     """Snapshot requested at P = L + off (P' = L): restore then re-prefill the
-    remainder [P', P + 32) equals the cold prefill bit for bit."""
+    remainder [P', P + 32) equals the cold prefill bit for bit; the cold run
+    itself matches the oracle (o over [P', P + 32) and every layer's final
+    state, max relative error 2e-3)."""
     w = ALIGN
     P = L + off
     F = P + 32
@@ -105,6 +139,40 @@ def test_alignment_sweep(inputs_align, L, off):
     warm.poison()
     assert warm.restore(c, d) == L
     warm.prefill(L, F)
+    torch.cuda.synchronize()
+    assert_same_outputs(cold, warm, L, F)
+    errs = []
+    for l in range(w.n_linear):
+        e_o = rel_err(cold.o[l][L:F].cpu().numpy(), oracle_align[l]["o"][L:F])
+        e_s = rel_err(cold.state[l].cpu().numpy(), oracle_state_at(orc, inputs_align, oracle_align, l, F))
+        errs.append(max(e_o, e_s))
+    print("L %d off %d: max rel err vs oracle over 6 layers %.3g" % (L, off, max(errs)))
+    assert max(errs) <= PARITY_TOL
+
+
+@pytest.mark.parametrize("mixer", ["linattn", "gdn"])
+def test_one_token_remainder_then_decode(inputs_hyb8, mixer):
+    """A snapshot requested one token past a chunk boundary (P = P' + 1):
+    restore P', re-prefill the one-token remainder as its own call, then
+    decode -- equal bit for bit to a cold session that prefilled [0, P) in
+    one call and decoded the same tokens."""
+    w = HYB8
+    L, n = 2048, 4
+    P = L + 1
+    F = P + n
+    inp = inputs_hyb8 if mixer == "linattn" else make_inputs(w, F, w.seed + 5, mixer)
+    cold = HybridStack(w, F, inputs=inp, mixer=mixer)
+    cold.prefill(0, P)
+    cold.decode(n)
+    warm = HybridStack(w, F, inputs=inp, mixer=mixer)
+    warm.prefill(0, L)
+    d = digest_of(w, P)
+    c = warm.snapshot(P, d)
+    warm.prefill(L, P)
+    warm.poison()
+    assert warm.restore(c, d) == L
+    warm.prefill(L, P)   # the remainder: one token, one call
+    warm.decode(n)
     torch.cuda.synchronize()
     assert_same_outputs(cold, warm, L, F)
 

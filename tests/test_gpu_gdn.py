@@ -188,10 +188,11 @@ def test_gdn_workspace_is_caller_owned(orc):
 
 @pytest.mark.parametrize("dk,dv", [(128, 128), (64, 32)])
 def test_gdn_one_token_agrees_with_chunked(dk, dv):
-    """A one-token call (the decode path, one launch) continues from a chunk
-    boundary like the chunked kernel's one-token chunk: token 64 of one
-    65-token call against a one-token call from that call's chunk state 1 --
-    state and o equal to fp32 rounding, chunk state 0 = the entering state."""
+    """A one-token prefill from a chunk boundary is the chunked path's
+    one-token chunk: token 64 of one 65-token call against a one-token call
+    from that call's chunk state 1 -- state and o equal bit for bit, chunk
+    state 0 = the entering state.  The decode step (one launch, no workspace)
+    agrees to fp32 rounding."""
     import torch
     T, H = 65, 4
     inp = gdn_case(47, T, H, dk, dv)
@@ -204,10 +205,16 @@ def test_gdn_one_token_agrees_with_chunked(dk, dv):
     fs1 = torch.empty((H, dk, dv), dtype=torch.float32, device="cuda")
     cap.gdn_chunked_prefill(d["q"][64:], d["k"][64:], d["v"][64:], d["g"][64:], d["beta"][64:], o1, state_in=st,
                             chunk_states=cs1, final_state=fs1, T=1, H=H, dk=dk, dv=dv)
+    o2 = torch.empty((1, H, dv), dtype=torch.float32, device="cuda")
+    fs2 = torch.empty((H, dk, dv), dtype=torch.float32, device="cuda")
+    cap.gdn_decode_step(d["q"][64:], d["k"][64:], d["v"][64:], d["g"][64:], d["beta"][64:], o2, state_in=st,
+                        final_state=fs2, T=1, H=H, dk=dk, dv=dv)
     torch.cuda.synchronize()
     assert np.array_equal(cs1.cpu().numpy()[0], cs[1])
-    assert rel_err(fs1.cpu().numpy(), fs) <= SPLIT_TOL
-    assert rel_err(o1.cpu().numpy()[0], o[64]) <= SPLIT_TOL
+    assert np.array_equal(fs1.cpu().numpy(), fs)
+    assert np.array_equal(o1.cpu().numpy()[0], o[64])
+    assert rel_err(fs2.cpu().numpy(), fs) <= SPLIT_TOL
+    assert rel_err(o2.cpu().numpy()[0], o[64]) <= SPLIT_TOL
 
 
 @pytest.mark.parametrize("gv,bv", [(-100.0, None), (None, 0.0), (None, 1.0)])
@@ -226,8 +233,12 @@ def test_gdn_one_token_extremes_and_inplace(orc, gv, bv):
     st = torch.from_numpy(S0).cuda()
     o = torch.empty((1, H, dv), dtype=torch.float32, device="cuda")
     cap.gdn_chunked_prefill(d["q"], d["k"], d["v"], d["g"], d["beta"], o, state_in=st, final_state=st)
+    st2 = torch.from_numpy(S0).cuda()
+    o2 = torch.empty((1, H, dv), dtype=torch.float32, device="cuda")
+    cap.gdn_decode_step(d["q"], d["k"], d["v"], d["g"], d["beta"], o2, state_in=st2, final_state=st2)
     torch.cuda.synchronize()
     o_ref, s_ref = orc.gdn_sequential(inp["q"], inp["k"], inp["v"], inp["g"], inp["beta"], S0=S0)
-    e = (rel_err(o.cpu().numpy(), o_ref), rel_err(st.cpu().numpy(), s_ref))
-    print("  g %s beta %s: rel err o %.3g state %.3g" % ((gv, bv) + e), flush=True)
+    e = (rel_err(o.cpu().numpy(), o_ref), rel_err(st.cpu().numpy(), s_ref),
+         rel_err(o2.cpu().numpy(), o_ref), rel_err(st2.cpu().numpy(), s_ref))
+    print("  g %s beta %s: rel err o %.3g state %.3g (decode step: o %.3g state %.3g)" % ((gv, bv) + e), flush=True)
     assert max(e) <= SPLIT_TOL, e

@@ -101,6 +101,12 @@ def test_scan_optional_outputs_and_inplace(orc):
     cap.linattn_chunked_prefill(d["q"], d["k"], d["v"], d["g"], o, state_in=st, final_state=st)
     torch.cuda.synchronize()
     assert np.array_equal(o.cpu().numpy(), o_a) and np.array_equal(st.cpu().numpy(), fs_a)
+    # the decode step in place: the same state bits, o to fp32 rounding
+    st2 = torch.from_numpy(S0).cuda()
+    o2 = torch.empty((1, H, dv), dtype=torch.float32, device="cuda")
+    cap.linattn_decode_step(d["q"], d["k"], d["v"], d["g"], o2, state_in=st2, final_state=st2)
+    torch.cuda.synchronize()
+    assert np.array_equal(st2.cpu().numpy(), fs_a) and rel_err(o2.cpu().numpy(), o_a) <= SPLIT_TOL
 
 
 def test_scan_scale(orc):
@@ -150,10 +156,11 @@ def test_aligned_continuation_bitwise(P):
 
 @pytest.mark.parametrize("dk,dv", [(128, 128), (64, 32)])
 def test_one_token_state_equals_chunked_fold(dk, dv):
-    """A one-token call (the decode path) folds the state exactly as the
-    chunked kernel folds a one-token chunk: the state after token 64 of one
-    65-token call equals, bit for bit, a one-token call from that call's
-    chunk-boundary state 1; o of that token agrees to fp32 rounding."""
+    """A one-token prefill from a chunk boundary is the chunked kernel's
+    one-token chunk: token 64 of one 65-token call against a one-token call
+    from that call's chunk-boundary state 1 -- o and the state equal bit for
+    bit.  The decode step (vector-ALU path) folds the state bit-identically
+    and agrees on o to fp32 rounding."""
     import torch
     T, H = 65, 4
     inp = scan_case(41, T, H, dk, dv)
@@ -167,10 +174,29 @@ def test_one_token_state_equals_chunked_fold(dk, dv):
     cap.linattn_chunked_prefill(d["q"][64:], d["k"][64:], d["v"][64:], d["g"][64:], o1, state_in=st,
                                 chunk_states=cs1, final_state=fs1, T=1, H=H, dk=dk, dv=dv,
                                 in_dtype=cap.CAP_DTYPE_BF16)
+    o2 = torch.empty((1, H, dv), dtype=torch.float32, device="cuda")
+    fs2 = torch.empty((H, dk, dv), dtype=torch.float32, device="cuda")
+    cap.linattn_decode_step(d["q"][64:], d["k"][64:], d["v"][64:], d["g"][64:], o2, state_in=st,
+                            final_state=fs2, T=1, H=H, dk=dk, dv=dv, in_dtype=cap.CAP_DTYPE_BF16)
     torch.cuda.synchronize()
     assert np.array_equal(fs1.cpu().numpy(), fs)
     assert np.array_equal(cs1.cpu().numpy()[0], cs[1])  # entry 0 is the state entering the call
-    assert rel_err(o1.cpu().numpy()[0], o[64]) <= SPLIT_TOL
+    assert np.array_equal(o1.cpu().numpy()[0], o[64])
+    assert np.array_equal(fs2.cpu().numpy(), fs)
+    assert rel_err(o2.cpu().numpy()[0], o[64]) <= SPLIT_TOL
+
+
+def test_decode_step_argument_checks():
+    """The decode step takes exactly one token."""
+    import torch
+    H, dk, dv = 2, 128, 16
+    inp = scan_case(45, 2, H, dk, dv)
+    d = dev_inputs(inp)
+    o = torch.empty((2, H, dv), dtype=torch.float32, device="cuda")
+    for T in (0, 2):
+        with pytest.raises(cap.CapsuleError) as ei:
+            cap.linattn_decode_step(d["q"], d["k"], d["v"], d["g"], o, T=T, H=H, dk=dk, dv=dv)
+        assert ei.value.status == cap.CAP_E_UNSUPPORTED
 
 
 def test_one_token_inplace_and_optional_outputs(orc):
@@ -189,6 +215,12 @@ def test_one_token_inplace_and_optional_outputs(orc):
     cap.linattn_chunked_prefill(d["q"], d["k"], d["v"], d["g"], o, state_in=st, final_state=st)
     torch.cuda.synchronize()
     assert np.array_equal(o.cpu().numpy(), o_a) and np.array_equal(st.cpu().numpy(), fs_a)
+    # the decode step in place: the same state bits, o to fp32 rounding
+    st2 = torch.from_numpy(S0).cuda()
+    o2 = torch.empty((1, H, dv), dtype=torch.float32, device="cuda")
+    cap.linattn_decode_step(d["q"], d["k"], d["v"], d["g"], o2, state_in=st2, final_state=st2)
+    torch.cuda.synchronize()
+    assert np.array_equal(st2.cpu().numpy(), fs_a) and rel_err(o2.cpu().numpy(), o_a) <= SPLIT_TOL
     o_z, cs_z, fs_z = _run(inp, 1, H, dk, dv)
     o_ref, s_ref = orc.sequential(inp["q"], inp["k"], inp["v"], inp["g"])
     assert not cs_z.any() and rel_err(o_z, o_ref) <= SPLIT_TOL and rel_err(fs_z, s_ref) <= SPLIT_TOL

@@ -101,12 +101,6 @@ def test_scan_optional_outputs_and_inplace(orc):
     cap.linattn_chunked_prefill(d["q"], d["k"], d["v"], d["g"], o, state_in=st, final_state=st)
     torch.cuda.synchronize()
     assert np.array_equal(o.cpu().numpy(), o_a) and np.array_equal(st.cpu().numpy(), fs_a)
-    # the decode step in place: the same state bits, o to fp32 rounding
-    st2 = torch.from_numpy(S0).cuda()
-    o2 = torch.empty((1, H, dv), dtype=torch.float32, device="cuda")
-    cap.linattn_decode_step(d["q"], d["k"], d["v"], d["g"], o2, state_in=st2, final_state=st2)
-    torch.cuda.synchronize()
-    assert np.array_equal(st2.cpu().numpy(), fs_a) and rel_err(o2.cpu().numpy(), o_a) <= SPLIT_TOL
 
 
 def test_scan_scale(orc):

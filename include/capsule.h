@@ -371,6 +371,32 @@ CAP_API int gdn_chunked_prefill(const gdn_args* args, void* stream);
  * rounding; decode steps are reproducible among themselves. */
 CAP_API int gdn_decode_step(const gdn_args* args, void* stream);
 
+/* ---------------------------- delta-rule prefill without allocation ---- */
+/* For callers that cannot allocate device memory or hand in a workspace:
+ * code recorded under stream capture (a HIP graph), tight serving loops,
+ * harnesses that forbid allocation.  gdn_chunked_prefill with its
+ * per-chunk workspace held in a fixed device array that the library owns:
+ * GDN_NOALLOC_SCRATCH_BYTES on every GPU the library runs on, held until the
+ * process ends.  The array keeps two states of all heads (the hand-over
+ * between segments) and as many per-(chunk, head) workspace records as fit;
+ * a call whose chunks do not all fit runs as several segments of whole
+ * chunks (a prepare and a scan launch each), which computes exactly what one
+ * gdn_chunked_prefill call computes (bit for bit: a chunk depends only on
+ * the state entering it and its inputs).  Nothing is allocated: no
+ * hipMalloc, no host heap.
+ *
+ * Arguments as gdn_chunked_prefill, except that workspace must be NULL and
+ * workspace_bytes 0 (CAP_E_INVAL otherwise).  CAP_E_SIZE when one chunk of
+ * all heads plus the two states does not fit the array:
+ * 2 * round_up(H * dk * dv * 4, 256) + H * 12800 > GDN_NOALLOC_SCRATCH_BYTES
+ * (H <= 233 at dk = dv = 128).  Every call on one GPU shares that GPU's
+ * array (it keeps the last call's contents, which no call reads before
+ * writing): calls that may overlap on one GPU -- on different streams, or
+ * from several threads -- race and must be serialised by the caller. */
+#define GDN_NOALLOC_SCRATCH_BYTES (32ull << 20)
+
+CAP_API int gdn_chunked_prefill_noalloc(const gdn_args* args, void* stream);
+
 /* ---------------------------------------------------------- FP8 KV ------ */
 /* §3 "Definition": the KV region may be held in FP8, which roughly halves
  * the capsule (an FP8 K or V buffer is an ordinary POSITIONAL buffer with

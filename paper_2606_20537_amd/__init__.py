@@ -12,6 +12,7 @@ from ._native import (  # noqa: F401
     cap_set_destroy, cap_set_get_position, cap_set_set_position, cap_status_string, capsule_bytes,
     capsule_digest_tokens, capsule_fork, capsule_gather_restore, capsule_info, capsule_layout_bytes,
     capsule_move, capsule_release, capsule_restore, capsule_snapshot, capsule_tier, gdn_chunked_prefill,
+    gdn_chunked_prefill_noalloc, GDN_NOALLOC_SCRATCH_BYTES,
     gdn_decode_step, gdn_workspace_bytes, kv_fp8_dequantize, kv_fp8_quantize, linattn_chunked_prefill,
     linattn_decode_step, load,
 )

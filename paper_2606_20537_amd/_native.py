@@ -95,6 +95,7 @@ SIGNATURES = [
     ("gdn_workspace_bytes", _u64, [ct.c_int64, _i32, _i32]),
     ("gdn_chunked_prefill", ct.c_int, [ct.POINTER(gdn_args), _vp]),
     ("gdn_decode_step", ct.c_int, [ct.POINTER(gdn_args), _vp]),
+    ("gdn_chunked_prefill_noalloc", ct.c_int, [ct.POINTER(gdn_args), _vp]),
 ]
 
 _lib = None
@@ -374,6 +375,23 @@ def gdn_chunked_prefill(q, k, v, g, beta, o, *, state_in=None, chunk_states=None
                  _addr(chunk_states), _addr(final_state), _addr(workspace), int(workspace_bytes), int(T), int(H),
                  int(dk), int(dv), int(chunk), int(in_dtype), float(scale))
     return _check("gdn_chunked_prefill", load().gdn_chunked_prefill(ct.byref(a), _stream(stream)))
+
+
+GDN_NOALLOC_SCRATCH_BYTES = 32 << 20
+
+
+def gdn_chunked_prefill_noalloc(q, k, v, g, beta, o, *, state_in=None, chunk_states=None, final_state=None,
+                                T=None, H=None, dk=None, dv=None, chunk=64, in_dtype=CAP_DTYPE_BF16, scale=1.0,
+                                stream=None):
+    """gdn_chunked_prefill with the library's own device scratch: no
+    workspace argument, nothing allocated."""
+    if T is None:
+        T, H, dk = q.shape
+        dv = v.shape[2]
+    a = gdn_args(_addr(q), _addr(k), _addr(v), _addr(g), _addr(beta), _addr(state_in), _addr(o),
+                 _addr(chunk_states), _addr(final_state), 0, 0, int(T), int(H), int(dk), int(dv), int(chunk),
+                 int(in_dtype), float(scale))
+    return _check("gdn_chunked_prefill_noalloc", load().gdn_chunked_prefill_noalloc(ct.byref(a), _stream(stream)))
 
 
 def gdn_decode_step(q, k, v, g, beta, o, *, state_in=None, final_state=None, T=None, H=None, dk=None, dv=None,

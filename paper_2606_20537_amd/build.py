@@ -10,7 +10,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB_PATH = os.path.join(PKG, "_build", "libcapsule.so")
-SOURCES = ["capsule_host.cpp", "capsule_copy.hip", "linattn_scan.hip", "linattn_step.hip", "gdn_scan.hip", "gdn_step.hip", "kv_fp8.hip", "append.hip"]
+SOURCES = ["capsule_host.cpp", "capsule_copy.hip", "linattn_scan.hip", "linattn_step.hip", "gdn_scan.hip", "gdn_step.hip", "gdn_noalloc.hip", "kv_fp8.hip", "append.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 # gfx950 only.  Packed-fp32 instructions are disabled for all device code.

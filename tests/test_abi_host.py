@@ -297,3 +297,27 @@ def test_fp8_argument_checks():
         two = [(1 << 20, 1 << 24, 1024, 1.0, 0), (1 << 21, (1 << 24) + 512, 1024, 1.0, 0)]
         assert _fp8_status(two, q) == cap.CAP_E_INVAL                                        # dst overlap
 
+
+
+def test_noalloc_argument_checks():
+    """The no-allocation delta-rule prefill: the prefill's checks, no
+    workspace argument, and CAP_E_SIZE when one chunk of all heads does not
+    fit its fixed scratch -- all on the host before any device call."""
+    L = N.load()
+    assert L.gdn_chunked_prefill_noalloc(None, None) == cap.CAP_E_INVAL
+    base = dict(q=4096, k=8192, v=12288, g=16384, beta=20480, state_in=0, o=1 << 30, chunk_states=0,
+                final_state=0, workspace=0, workspace_bytes=0, T=4, H=1, dk=64, dv=16, chunk=64,
+                in_dtype=cap.CAP_DTYPE_BF16, scale=1.0)
+
+    def st(**kw):
+        a = dict(base)
+        a.update(kw)
+        return L.gdn_chunked_prefill_noalloc(ct.byref(N.gdn_args(**a)), None)
+    assert st(workspace=1 << 31, workspace_bytes=12800) == cap.CAP_E_INVAL
+    assert st(workspace_bytes=16) == cap.CAP_E_INVAL
+    assert st(beta=0) == cap.CAP_E_INVAL
+    assert st(dk=96) == cap.CAP_E_UNSUPPORTED
+    assert st(T=0, q=0, k=0, v=0, g=0, beta=0, o=0, H=300, dk=128, dv=128) == cap.CAP_E_SIZE
+    assert st(T=0, q=0, k=0, v=0, g=0, beta=0, o=0, H=233, dk=128, dv=128) == cap.CAP_OK
+    assert st(T=0, q=0, k=0, v=0, g=0, beta=0, o=0, H=234, dk=128, dv=128) == cap.CAP_E_SIZE
+    assert cap.GDN_NOALLOC_SCRATCH_BYTES == 32 << 20

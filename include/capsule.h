@@ -402,8 +402,8 @@ CAP_API int gdn_chunked_prefill_noalloc(const gdn_args* args, void* stream);
  * the capsule (an FP8 K or V buffer is an ordinary POSITIONAL buffer with
  * one byte per element); the BF16 working stage read by the attention is not
  * part of the capsule and is rebuilt lazily after a restore (§3 cost model:
- * restore copies bytes and rebinds; the stage of a restored session is valid
- * over no rows until rebuilt with kv_fp8_dequantize).
+ * restore copies bytes and rebinds; the bound-stage calls below track which
+ * rows a session's stage holds and convert only the rows it lacks).
  *
  * Format: OCP 8-bit floating point E4M3 (sign, 4 exponent bits with bias 7,
  * 3 mantissa bits; largest finite 448; S.1111.111 is NaN; no infinities),
@@ -424,6 +424,61 @@ typedef struct kv_fp8_seg {
     float       scale;
     uint32_t    reserved;
 } kv_fp8_seg;
+
+/* ------------------------------------------- FP8 working stage (lazy) -- */
+/* §3 "Definition" counts the FP8 dequantisation stage's valid end in a
+ * capsule's KV region; §3 cost model and Table "cost structure": restore
+ * copies bytes back and re-binds, and the BF16 stage is rebuilt lazily on
+ * the next read, not eagerly in restore.
+ *
+ * A positional buffer of a set may hold FP8 rows (row_bytes = elements per
+ * row) and be bound to a BF16 working stage, caller-owned device memory of
+ * rows * row_bytes bf16 elements that the attention reads.  The set keeps
+ * one stage valid end E for all its stages: rows [0, E) of every bound
+ * stage hold the dequantisation (kv_fp8_dequantize) of the FP8 rows.
+ *   - cap_stage_acquire(set, n) is the read: it converts exactly rows
+ *     [E, n) of every stage in one launch (nothing when n <= E), then
+ *     E = max(E, n).
+ *   - capsule_snapshot records min(E, P') in the capsule (capsule_stage_end).
+ *   - capsule_restore re-binds E and converts nothing: restoring into the
+ *     set the capsule was taken from, in the same lineage -- no restore,
+ *     fork, gather, rebinding or invalidation of that set since the
+ *     snapshot, and no append below rows the set already held -- E becomes
+ *     min(E, the capsule's recorded end), since those stage rows are already
+ *     the dequantised capsule rows; in every other case E becomes 0.
+ *   - capsule_fork and capsule_gather_restore leave every destination at 0.
+ *   - cap_set_append below rows the set already held clips E to the append
+ *     position.
+ * The library assumes that bound stages, and the FP8 rows below a set's
+ * position, change only through these calls; a caller that writes either
+ * otherwise (filling the FP8 region itself, say) calls
+ * cap_stage_invalidate.  Stages belong to the live session, never to a
+ * capsule. */
+#define CAP_MAX_STAGES 64u   /* stages per set (one rebuild launch) */
+
+/* Bind buffer `buffer` (a POSITIONAL buffer of FP8 rows; CAP_E_UNSUPPORTED
+ * otherwise) to a stage of rows * row_bytes bf16 elements at `stage`
+ * (16-byte aligned, disjoint from every live buffer and every other stage of
+ * the set: CAP_E_ALIGN / CAP_E_INVAL), decoded with `scale` (finite, > 0).
+ * Binding a buffer again replaces its stage.  Sets E = 0.  Host only. */
+CAP_API int cap_set_bind_stage(cap_set set, uint32_t buffer, void* stage, float scale);
+
+/* The first read of rows [0, rows) of the stages: converts rows [E, rows) of
+ * every bound stage (kv_fp8_dequantize semantics) in one stream-ordered
+ * launch, sets E = max(E, rows) and returns the number of rows converted in
+ * *converted (may be NULL; 0 when rows <= E, and then nothing is enqueued).
+ * rows must not exceed the set's position (CAP_E_SIZE); a set with no bound
+ * stage is CAP_E_STATE. */
+CAP_API int cap_stage_acquire(cap_set set, uint64_t rows, void* stream, uint64_t* converted);
+
+/* E of a set. */
+CAP_API int cap_stage_valid_end(cap_set set, uint64_t* end);
+
+/* E = 0 and a new lineage (after the caller wrote a stage or FP8 rows itself). */
+CAP_API int cap_stage_invalidate(cap_set set);
+
+/* The stage valid end a capsule recorded (min(E, P') at its snapshot). */
+CAP_API int capsule_stage_end(cap_capsule cap, uint64_t* end);
 
 /* bf16 -> E4M3: code = nearest representable value to float(x) * (1.0f /
  * scale) (fp32 product), ties to the even mantissa; |value| >= 448 and +-inf

@@ -32,6 +32,7 @@ CAP_DTYPE_BF16 = 1
 CAP_MAX_BUFFERS = 512
 CAP_MAX_FORK = 16
 CAP_MAX_GALLERY = 64
+CAP_MAX_STAGES = 64
 
 
 class CapsuleError(RuntimeError):
@@ -88,6 +89,11 @@ SIGNATURES = [
     ("kv_fp8_quantize", ct.c_int, [ct.POINTER(kv_fp8_seg), _u32, _vp]),
     ("kv_fp8_dequantize", ct.c_int, [ct.POINTER(kv_fp8_seg), _u32, _vp]),
     ("capsule_tier", ct.c_int, [_vp, ct.POINTER(_u32)]),
+    ("cap_set_bind_stage", ct.c_int, [_vp, _u32, _vp, ct.c_float]),
+    ("cap_stage_acquire", ct.c_int, [_vp, _u64, _vp, ct.POINTER(_u64)]),
+    ("cap_stage_valid_end", ct.c_int, [_vp, ct.POINTER(_u64)]),
+    ("cap_stage_invalidate", ct.c_int, [_vp]),
+    ("capsule_stage_end", ct.c_int, [_vp, ct.POINTER(_u64)]),
     ("capsule_release", ct.c_int, [_vp]),
     ("capsule_digest_tokens", _u64, [ct.POINTER(_i32), _u64]),
     ("linattn_chunked_prefill", ct.c_int, [ct.POINTER(linattn_args), _vp]),
@@ -304,6 +310,35 @@ def capsule_move(cap, arena, arena_bytes=None, stream=None):
 def capsule_tier(cap):
     out = _u32(0)
     _check("capsule_tier", load().capsule_tier(cap.handle, ct.byref(out)))
+    return int(out.value)
+
+
+def cap_set_bind_stage(s, buffer, stage, scale):
+    """Bind FP8 positional buffer ``buffer`` (index in the set) to a bf16
+    working stage (tensor or address) decoded with ``scale``."""
+    return _check("cap_set_bind_stage", load().cap_set_bind_stage(s.handle, int(buffer), _addr(stage), float(scale)))
+
+
+def cap_stage_acquire(s, rows, stream=None):
+    """Make rows [0, rows) of the set's stages valid; returns the rows converted."""
+    out = _u64(0)
+    _check("cap_stage_acquire", load().cap_stage_acquire(s.handle, int(rows), _stream(stream), ct.byref(out)))
+    return int(out.value)
+
+
+def cap_stage_valid_end(s):
+    out = _u64(0)
+    _check("cap_stage_valid_end", load().cap_stage_valid_end(s.handle, ct.byref(out)))
+    return int(out.value)
+
+
+def cap_stage_invalidate(s):
+    return _check("cap_stage_invalidate", load().cap_stage_invalidate(s.handle))
+
+
+def capsule_stage_end(cap):
+    out = _u64(0)
+    _check("capsule_stage_end", load().capsule_stage_end(cap.handle, ct.byref(out)))
     return int(out.value)
 
 

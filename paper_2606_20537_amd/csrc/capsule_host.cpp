@@ -6,6 +6,7 @@
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
+#include <atomic>
 #include <memory>
 #include <stdexcept>
 #include <cmath>
@@ -29,6 +30,13 @@ struct BufInfo {
     uint32_t kind;
 };
 
+// A BF16 working stage bound to an FP8 positional buffer of a set.
+struct StageInfo {
+    uint32_t buf;     // index of the FP8 buffer in the set
+    uint64_t ptr;     // stage device address: rows x row_bytes bf16 elements
+    float scale;
+};
+
 struct cap_set_s {
     std::vector<BufInfo> bufs;
     uint32_t chunk = 1;
@@ -38,6 +46,17 @@ struct cap_set_s {
     SegEntry* dtab = nullptr;   // n + 1 entries on the device
     int device = 0;
     int num_cus = 256;
+    // FP8 working stages and their valid end: rows [0, stage_end) of every
+    // bound stage are the dequantised FP8 rows.  `epoch` names the lineage of
+    // the set's positional rows: it changes whenever rows the set already
+    // held may be replaced (restore, fork, gather into the set, an append
+    // below `high_water`, a rebinding); `high_water` is the end of the rows
+    // written in this lineage.
+    std::vector<StageInfo> stages;
+    uint64_t stage_end = 0;
+    uint64_t uid = 0;
+    uint64_t epoch = 0;
+    uint64_t high_water = 0;
 };
 
 struct cap_capsule_s {
@@ -51,6 +70,11 @@ struct cap_capsule_s {
     uint32_t tier = CAP_TIER_DEVICE;  // where the arena lives
     std::vector<uint64_t> row_bytes, rows;
     std::vector<uint32_t> kinds;
+    // the FP8 stage's valid end at the snapshot (clipped to P'), and the
+    // set and lineage it was recorded in
+    uint64_t stage_end = 0;
+    uint64_t set_uid = 0;
+    uint64_t epoch = 0;
 };
 
 namespace {
@@ -72,6 +96,18 @@ int guarded(F&& body) noexcept {
 }
 
 bool aligned16(uint64_t x) { return (x & 15u) == 0; }
+
+// Process-wide counter for set identities and lineage epochs.
+std::atomic<uint64_t> g_ids{1};
+uint64_t next_id() { return g_ids.fetch_add(1, std::memory_order_relaxed); }
+
+// The rows a set held may have been replaced: new lineage, stage valid over
+// no rows unless `keep` says otherwise.
+void new_lineage(cap_set_s* s, uint64_t keep_stage_end, uint64_t high_water) {
+    s->stage_end = keep_stage_end;
+    s->epoch = next_id();
+    s->high_water = high_water;
+}
 
 uint64_t buf_bytes(uint64_t row_bytes, uint64_t rows, uint32_t kind, uint64_t P) {
     return kind == CAP_KIND_POSITIONAL ? P * row_bytes : row_bytes * rows;
@@ -227,6 +263,8 @@ int cap_set_create(const cap_buf* bufs, uint32_t n, uint32_t chunk, uint64_t dep
         s->chunk = chunk;
         s->deploy_key = deploy_key;
         s->max_position = UINT64_MAX;
+        s->uid = next_id();
+        s->epoch = next_id();
         std::vector<SegEntry> tab(n + 1);
         uint64_t a = 0, b = 0;
         for (uint32_t i = 0; i < n; ++i) {
@@ -327,6 +365,9 @@ int capsule_snapshot(cap_set live, uint64_t P, uint64_t prefix_digest, void* are
             c->rows.push_back(b.rows);
             c->kinds.push_back(b.kind);
         }
+        c->stage_end = std::min(live->stage_end, Pa);
+        c->set_uid = live->uid;
+        c->epoch = live->epoch;
 
         cap::CopyParams p{};
         p.layout = live->dtab;
@@ -367,6 +408,11 @@ int capsule_restore(cap_capsule cap, cap_set live, uint64_t prefix_digest, void*
         rc = launch_status(cap::launch_copy(p, live->num_cus, static_cast<hipStream_t>(stream)));
         if (rc != CAP_OK) return rc;
         live->position = cap->P_aligned;
+        // re-bind the FP8 stage (nothing is converted here): in the set and
+        // lineage the capsule was taken from, the stage rows below the
+        // recorded end are still the dequantised capsule rows
+        const bool same = cap->set_uid == live->uid && cap->epoch == live->epoch;
+        new_lineage(live, same ? std::min(live->stage_end, cap->stage_end) : 0, cap->P_aligned);
         if (P_restored) *P_restored = cap->P_aligned;
         return CAP_OK;
     });
@@ -413,7 +459,10 @@ int capsule_fork(cap_capsule cap, const cap_set* lives, uint32_t n, uint64_t pre
             rc = launch_status(cap::launch_copy(p, lives[0]->num_cus, static_cast<hipStream_t>(stream)));
             if (rc != CAP_OK) return rc;
         }
-        for (uint32_t i = 0; i < n; ++i) lives[i]->position = cap->P_aligned;
+        for (uint32_t i = 0; i < n; ++i) {
+            lives[i]->position = cap->P_aligned;
+            new_lineage(lives[i], 0, cap->P_aligned);
+        }
         return CAP_OK;
     });
 }
@@ -477,7 +526,10 @@ int capsule_gather_restore(const cap_capsule* gallery, uint32_t n_gallery, const
             rc = launch_status(cap::launch_copy(p, lives[0]->num_cus, static_cast<hipStream_t>(stream)));
             if (rc != CAP_OK) return rc;
         }
-        for (uint32_t e = 0; e < n_env; ++e) lives[e]->position = c0->P_aligned;
+        for (uint32_t e = 0; e < n_env; ++e) {
+            lives[e]->position = c0->P_aligned;
+            new_lineage(lives[e], 0, c0->P_aligned);
+        }
         return CAP_OK;
     });
 }
@@ -586,7 +638,12 @@ int cap_set_append(cap_set live, const void* const* srcs, uint64_t n, void* stre
             rc = launch_status(cap::launch_append(p, static_cast<hipStream_t>(stream)));
             if (rc != CAP_OK) return rc;
         }
+        // rows below the high-water mark rewritten: a new lineage, and the
+        // stage keeps only the rows below the append
+        if (n > 0 && live->position < live->high_water)
+            new_lineage(live, std::min(live->stage_end, live->position), live->high_water);
         live->position += n;
+        live->high_water = live->position;
         return CAP_OK;
     });
 }
@@ -639,6 +696,84 @@ int kv_fp8_quantize(const kv_fp8_seg* segs, uint32_t n_seg, void* stream) {
 
 int kv_fp8_dequantize(const kv_fp8_seg* segs, uint32_t n_seg, void* stream) {
     return fp8_convert(segs, n_seg, stream, false);
+}
+
+// ------------------------------------------------ FP8 working stage ----
+int cap_set_bind_stage(cap_set set, uint32_t buffer, void* stage, float scale) {
+    return guarded([&]() -> int {
+        if (!set || !stage) return CAP_E_INVAL;
+        if (buffer >= set->bufs.size()) return CAP_E_INVAL;
+        if (!(scale > 0.0f) || !std::isfinite(scale)) return CAP_E_INVAL;
+        const BufInfo& b = set->bufs[buffer];
+        if (b.kind != CAP_KIND_POSITIONAL) return CAP_E_UNSUPPORTED;
+        if (!aligned16((uint64_t)(uintptr_t)stage)) return CAP_E_ALIGN;
+        const uint64_t s0 = (uint64_t)(uintptr_t)stage;
+        if (b.rows * b.row_bytes > UINT64_MAX / 2) return CAP_E_SIZE;
+        const uint64_t s1 = s0 + 2 * b.rows * b.row_bytes;
+        for (const BufInfo& o : set->bufs)
+            if (overlaps(s0, s1, o.ptr, o.ptr + o.row_bytes * o.rows)) return CAP_E_INVAL;
+        bool replace = false;
+        for (const StageInfo& t : set->stages) {
+            if (t.buf == buffer) { replace = true; continue; }
+            const BufInfo& tb = set->bufs[t.buf];
+            if (overlaps(s0, s1, t.ptr, t.ptr + 2 * tb.rows * tb.row_bytes)) return CAP_E_INVAL;
+        }
+        if (!replace && set->stages.size() >= CAP_MAX_STAGES) return CAP_E_UNSUPPORTED;
+        if (replace) {
+            for (StageInfo& t : set->stages)
+                if (t.buf == buffer) t = StageInfo{buffer, s0, scale};
+        } else {
+            set->stages.push_back(StageInfo{buffer, s0, scale});
+        }
+        new_lineage(set, 0, set->high_water);  // the bound stages hold nothing yet
+        return CAP_OK;
+    });
+}
+
+int cap_stage_acquire(cap_set set, uint64_t rows, void* stream, uint64_t* converted) {
+    return guarded([&]() -> int {
+        if (!set) return CAP_E_INVAL;
+        if (set->stages.empty()) return CAP_E_STATE;
+        if (rows > set->position) return CAP_E_SIZE;
+        if (converted) *converted = 0;
+        if (rows <= set->stage_end) return CAP_OK;
+        int rc = current_device_matches(set);
+        if (rc != CAP_OK) return rc;
+        const uint64_t e0 = set->stage_end;
+        std::vector<kv_fp8_seg> segs;
+        for (const StageInfo& t : set->stages) {
+            const BufInfo& b = set->bufs[t.buf];
+            kv_fp8_seg g{};
+            g.src = reinterpret_cast<const void*>(b.ptr + e0 * b.row_bytes);
+            g.dst = reinterpret_cast<void*>(t.ptr + 2 * e0 * b.row_bytes);
+            g.n = (rows - e0) * b.row_bytes;
+            g.scale = t.scale;
+            segs.push_back(g);
+        }
+        rc = fp8_convert(segs.data(), (uint32_t)segs.size(), stream, false);
+        if (rc != CAP_OK) return rc;
+        set->stage_end = rows;
+        if (converted) *converted = rows - e0;
+        return CAP_OK;
+    });
+}
+
+int cap_stage_valid_end(cap_set set, uint64_t* end) {
+    if (!set || !end) return CAP_E_INVAL;
+    *end = set->stage_end;
+    return CAP_OK;
+}
+
+int cap_stage_invalidate(cap_set set) {
+    if (!set) return CAP_E_INVAL;
+    new_lineage(set, 0, set->high_water);
+    return CAP_OK;
+}
+
+int capsule_stage_end(cap_capsule cap, uint64_t* end) {
+    if (!cap || !end) return CAP_E_INVAL;
+    *end = cap->stage_end;
+    return CAP_OK;
 }
 
 uint64_t capsule_digest_tokens(const int32_t* ids, uint64_t n) {

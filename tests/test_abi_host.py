@@ -126,6 +126,12 @@ def test_null_handles():
     assert L.capsule_move(None, None, 0, None, None) == cap.CAP_E_INVAL
     t = ct.c_uint32(9)
     assert L.capsule_tier(None, ct.byref(t)) == cap.CAP_E_INVAL and t.value == 9
+    e = ct.c_uint64(0)
+    assert L.cap_set_bind_stage(None, 0, None, ct.c_float(1.0)) == cap.CAP_E_INVAL
+    assert L.cap_stage_acquire(None, 0, None, None) == cap.CAP_E_INVAL
+    assert L.cap_stage_valid_end(None, ct.byref(e)) == cap.CAP_E_INVAL
+    assert L.cap_stage_invalidate(None) == cap.CAP_E_INVAL
+    assert L.capsule_stage_end(None, ct.byref(e)) == cap.CAP_E_INVAL
 
 
 def _args(**kw):

@@ -20,7 +20,7 @@
 // therefore a software pipeline over chunks with one LDS barrier per step;
 // in step c:
 //   state waves 4-7  issue the HBM loads of chunk c+4, stage chunk c+2 in LDS
-//                    (K; the gate wave also V, V w and the decay tables),
+//                    (K; wave 4 also V and V w, wave 5 the decay tables),
 //                    start D_{c+1} on MFMA, write the chunk-boundary state
 //                    S_c, then S_{c+1} = exp(G_last) S_c + D_c (one FMA per
 //                    element) and publish S_{c+1} for step c+1;
@@ -184,8 +184,16 @@ struct Ctx {
 // same per-chunk code with a single barrier in both roles.
 
 // ------------------------------------------------------------- state role
-template <int DK, bool F32, bool ONE, bool TABLES>
+// Every state wave stages its share of K, folds and publishes its rows of
+// S.  In addition the V wave (wave 4, VW) loads and stages V and V w (with
+// its own gate scan for w) and issues the cooperative L2 prefetch, and the
+// gate wave (wave 5: wq == 1 of the plain instantiation, a wave-uniform
+// branch) loads the gates and writes the chunk's decay tables.  Waves 5-7
+// share one instantiation: a separate one for the gate wave measured 10 %
+// slower with the same arithmetic.
+template <int DK, bool F32, bool ONE, bool VW>
 __device__ __forceinline__ void state_role(const ScanParams& p, Smem<DK, F32>& sm, const Ctx& x, int wq) {
+    const bool GW = !VW && wq == 1;  // wave-uniform
     using S_ = Smem<DK, F32>;
     constexpr int KP = S_::KP;
     constexpr int NL = S_::NL;
@@ -225,21 +233,24 @@ __device__ __forceinline__ void state_role(const ScanParams& p, Smem<DK, F32>& s
             const int d0 = (pc % (DK / 8)) * 8;
             load_piece<F32>(R.kp[u], rk, (uint32_t)(m * x.qk_row + ((int64_t)h * DK + d0) * ES));
         }
-        if constexpr (TABLES) {
-            // V slice (lane l: rows l/2 and 32 + l/2, columns 8 (l%2)..+7)
-            // and the log-gates (lane t: token t) -- loaded by one wave only,
-            // so no two waves wait on the same cache lines
+        if constexpr (VW) {
+            // V slice (lane l: rows l/2 and 32 + l/2, columns 8 (l%2)..+7),
+            // loaded by one wave only, so no two waves wait on the same lines
             const rsrc_t rv = make_rsrc(static_cast<const char*>(p.v) + t0 * x.v_row, rows * x.v_row);
             #pragma unroll
             for (int i = 0; i < 2; ++i)
                 load_piece<F32>(R.vp[i], rv, (uint32_t)(((lane >> 1) + 32 * i) * x.v_row +
                                                         ((int64_t)h * dv + j0 + 8 * (lane & 1)) * ES));
+        }
+        if (VW || GW) {
+            // the log-gates (lane t: token t)
             const rsrc_t rg = make_rsrc(p.g + t0 * H, rows * H * 4);
             R.g = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rg, (uint32_t)((lane * H + h) * 4), 0, 0));
         }
     };
 
-    // K rows of a chunk into LDS; the gate wave also V, V w and the decay tables.
+    // K rows of a chunk into LDS; the V wave also V and V w, the gate wave
+    // the decay tables.
     auto stage = [&](St& R, int bk, int bq) {
         #pragma unroll
         for (int u = 0; u < PK; ++u) {
@@ -251,10 +262,10 @@ __device__ __forceinline__ void state_role(const ScanParams& p, Smem<DK, F32>& s
             *reinterpret_cast<bf16x8*>(&sm.k[bk][0][m * KP + d0]) = hi;
                 if (F32) *reinterpret_cast<bf16x8*>(&sm.k[bk][NL - 1][m * KP + d0]) = lo;
         }
-        if constexpr (TABLES) {
-            // the gate wave scans the chunk's log-gates (lane t holds G_t),
-            // stages V and V w (lane l: rows l/2 and 32 + l/2, columns
-            // 8 (l%2)..+7) and writes the decay tables
+        if constexpr (VW) {
+            // the V wave scans the chunk's log-gates (lane t holds G_t) for
+            // w and stages V and V w (lane l: rows l/2 and 32 + l/2, columns
+            // 8 (l%2)..+7)
             const float xs = wave_inclusive_sum(R.g);
             const float glast = lane_value(xs, 63);
             const float wl = __expf(glast - xs);  // w_t = exp(G_last - G_t)
@@ -275,6 +286,10 @@ __device__ __forceinline__ void state_role(const ScanParams& p, Smem<DK, F32>& s
                 *reinterpret_cast<bf16x8*>(&sm.vw[bk][0][m * VP + jj]) = hi;
                 *reinterpret_cast<bf16x8*>(&sm.vw[bk][1][m * VP + jj]) = lo;
             }
+        }
+        if (GW) {
+            // the gate wave scans the same gates and writes the decay tables
+            const float xs = wave_inclusive_sum(R.g);
             float ge[4];
             #pragma unroll
             for (int M = 0; M < 4; ++M) ge[M] = lane_value(xs, 16 * M + 15);
@@ -329,7 +344,7 @@ __device__ __forceinline__ void state_role(const ScanParams& p, Smem<DK, F32>& s
     // Cooperative L2 prefetch.  The 16-column slices of a head all read the
     // head's full Q and K rows and share the 128-byte lines of V; fetched
     // at the same moment by every slice, each line costs every workgroup a
-    // full HBM latency.  So the gate wave of each slice touches its eighth
+    // full HBM latency.  So the V wave of each slice touches its eighth
     // of the head's lines PREFETCH chunks ahead of the regular loads (rows
     // 8 s + i/2 of Q and K, line i%2; rows 16 (s%4) + i of V, line s/4), and
     // the other slices' loads then hit in L2.  The fetched value is only
@@ -387,7 +402,7 @@ __device__ __forceinline__ void state_role(const ScanParams& p, Smem<DK, F32>& s
 
     // step c: loads of c+4, staging of c+2, D_{c+1}; S_c out; S_{c+1} in
     auto step = [&](int64_t c, int u, St& Rc, St& Rs, f32x4 (&Dn)[NDW], const f32x4 (&Dc)[NDW]) {
-        if constexpr (TABLES) prefetch(u & 1, c + PREFETCH);
+        if constexpr (VW) prefetch(u & 1, c + PREFETCH);
         load_chunk(Rc, c + 4);
         stage(Rs, u & 1, (u + 2) & 3);
         fold_delta((u + 1) & 1, Dn);
@@ -433,7 +448,7 @@ __device__ __forceinline__ void state_role(const ScanParams& p, Smem<DK, F32>& s
         step(c + 3, 3, R3, R1, D0, D1);
     }
     store_final();
-    if constexpr (TABLES) __asm__ volatile("" : : "v"(pf[0]), "v"(pf[1]));
+    if constexpr (VW) __asm__ volatile("" : : "v"(pf[0]), "v"(pf[1]));
     }
 }
 
@@ -671,10 +686,10 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
     x.v_row = (int64_t)x.H * x.dv * ES;
     x.o_row = (int64_t)x.H * x.dv * 4;
 
-    // Issue priority follows the step lengths: the V-and-gate wave (wave 4)
-    // has the longest step of the eight and arrives last at each barrier, the
-    // output waves come next, the other state waves finish first.
-    if (wave == 4) __builtin_amdgcn_s_setprio(3);
+    // Issue priority follows the step lengths: the V wave (4) and the gate
+    // wave (5) have the longest steps of the eight, the output waves come
+    // next, the two plain state waves finish first.
+    if (wave == 4 || wave == 5) __builtin_amdgcn_s_setprio(3);
     if (wave < 4) __builtin_amdgcn_s_setprio(1);
     switch (wave) {
         case 0: output_role<DK, F32, ONE, 0>(p, sm, x); break;

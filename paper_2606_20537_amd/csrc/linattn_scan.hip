@@ -20,7 +20,8 @@
 // therefore a software pipeline over chunks with one LDS barrier per step;
 // in step c:
 //   state waves 4-7  issue the HBM loads of chunk c+4, stage chunk c+2 in LDS
-//                    (K; wave 4 also V and V w, wave 5 the decay tables),
+//                    (K; wave 4 also V and V w; wave 5 writes the decay
+//                    tables and fold weights of chunk c+3),
 //                    start D_{c+1} on MFMA, write the chunk-boundary state
 //                    S_c, then S_{c+1} = exp(G_last) S_c + D_c (one FMA per
 //                    element) and publish S_{c+1} for step c+1;
@@ -105,6 +106,7 @@ struct alignas(16) Smem {
     alignas(16) float eG[4][CH];           // exp(G_t)
     alignas(16) float bm[4][CH];           // exp(G_e - G_m), e = last token of m's block
     alignas(16) float ai[4][CH][4];        // exp(G_i - G_e(M)) for 16-token blocks M below i's
+    alignas(16) float w[4][CH];            // w_t = exp(G_last - G_t), the fold weights
 };
 
 // 8 consecutive input elements of one row (16 B of bf16 or 32 B of fp32).
@@ -185,10 +187,12 @@ struct Ctx {
 
 // ------------------------------------------------------------- state role
 // Every state wave stages its share of K, folds and publishes its rows of
-// S.  In addition the V wave (wave 4, VW) loads and stages V and V w (with
-// its own gate scan for w) and issues the cooperative L2 prefetch, and the
-// gate wave (wave 5: wq == 1 of the plain instantiation, a wave-uniform
-// branch) loads the gates and writes the chunk's decay tables.  Waves 5-7
+// S.  In addition the V wave (wave 4, VW) loads and stages V and V w and
+// issues the cooperative L2 prefetch, and the gate wave (wave 5: wq == 1 of
+// the plain instantiation, a wave-uniform branch) is the only wave that
+// reads the gates -- 64 cache lines per chunk for 256 bytes, since g is
+// token-major -- and writes the decay tables and the fold weights w one
+// chunk ahead of the V wave, which reads its weights from LDS.  Waves 5-7
 // share one instantiation: a separate one for the gate wave measured 10 %
 // slower with the same arithmetic.
 template <int DK, bool F32, bool ONE, bool VW>
@@ -242,15 +246,35 @@ __device__ __forceinline__ void state_role(const ScanParams& p, Smem<DK, F32>& s
                 load_piece<F32>(R.vp[i], rv, (uint32_t)(((lane >> 1) + 32 * i) * x.v_row +
                                                         ((int64_t)h * dv + j0 + 8 * (lane & 1)) * ES));
         }
-        if (VW || GW) {
-            // the log-gates (lane t: token t)
+        if ((VW && ONE) || GW) {
+            // the log-gates (lane t: token t): the gate wave's, and the V
+            // wave's in a call of at most one chunk
             const rsrc_t rg = make_rsrc(p.g + t0 * H, rows * H * 4);
             R.g = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rg, (uint32_t)((lane * H + h) * 4), 0, 0));
         }
     };
 
-    // K rows of a chunk into LDS; the V wave also V and V w, the gate wave
-    // the decay tables.
+    // The gate wave's part for one chunk: the inclusive in-chunk sums of the
+    // gates (lane t holds G_t), the decay tables the output waves read, and
+    // the fold weights w_t = exp(G_last - G_t) for the V wave.
+    auto gate_tables = [&](const St& R, int bq) {
+        const float xs = wave_inclusive_sum(R.g);
+        const float glast = lane_value(xs, 63);
+        sm.w[bq][lane] = __expf(glast - xs);
+        float ge[4];
+        #pragma unroll
+        for (int M = 0; M < 4; ++M) ge[M] = lane_value(xs, 16 * M + 15);
+        const int blk = lane >> 4;
+        sm.G2[bq][lane] = xs * LOG2E;
+        sm.eG[bq][lane] = __expf(xs);
+        sm.bm[bq][lane] = __expf(ge[blk] - xs);
+        f32x4 a;
+        #pragma unroll
+        for (int M = 0; M < 4; ++M) a[M] = (M < blk) ? __expf(xs - ge[M]) : 0.0f;
+        *reinterpret_cast<f32x4*>(&sm.ai[bq][lane][0]) = a;
+    };
+
+    // K rows of a chunk into LDS; the V wave also V and V w.
     auto stage = [&](St& R, int bk, int bq) {
         #pragma unroll
         for (int u = 0; u < PK; ++u) {
@@ -263,17 +287,21 @@ __device__ __forceinline__ void state_role(const ScanParams& p, Smem<DK, F32>& s
                 if (F32) *reinterpret_cast<bf16x8*>(&sm.k[bk][NL - 1][m * KP + d0]) = lo;
         }
         if constexpr (VW) {
-            // the V wave scans the chunk's log-gates (lane t holds G_t) for
-            // w and stages V and V w (lane l: rows l/2 and 32 + l/2, columns
-            // 8 (l%2)..+7)
-            const float xs = wave_inclusive_sum(R.g);
-            const float glast = lane_value(xs, 63);
-            const float wl = __expf(glast - xs);  // w_t = exp(G_last - G_t)
+            // the V wave stages V and V w (lane l: rows l/2 and 32 + l/2,
+            // columns 8 (l%2)..+7) with the weights the gate wave published
+            // a step earlier; in a call of at most one chunk it computes
+            // them itself, with the gate wave's instructions (same bits)
+            float wl = 0.0f;
+            if constexpr (ONE) {
+                const float xs = wave_inclusive_sum(R.g);
+                const float glast = lane_value(xs, 63);
+                wl = __expf(glast - xs);
+            }
             #pragma unroll
             for (int i = 0; i < 2; ++i) {
                 const int m = (lane >> 1) + 32 * i;
                 const int jj = 8 * (lane & 1);
-                const float wm = __shfl(wl, m, 64);
+                const float wm = ONE ? __shfl(wl, m, 64) : sm.w[bq][m];
                 float f[8];
                 piece_f32<F32>(R.vp[i], f);
                 bf16x8 hi, lo;
@@ -286,21 +314,6 @@ __device__ __forceinline__ void state_role(const ScanParams& p, Smem<DK, F32>& s
                 *reinterpret_cast<bf16x8*>(&sm.vw[bk][0][m * VP + jj]) = hi;
                 *reinterpret_cast<bf16x8*>(&sm.vw[bk][1][m * VP + jj]) = lo;
             }
-        }
-        if (GW) {
-            // the gate wave scans the same gates and writes the decay tables
-            const float xs = wave_inclusive_sum(R.g);
-            float ge[4];
-            #pragma unroll
-            for (int M = 0; M < 4; ++M) ge[M] = lane_value(xs, 16 * M + 15);
-            const int blk = lane >> 4;
-            sm.G2[bq][lane] = xs * LOG2E;
-            sm.eG[bq][lane] = __expf(xs);
-            sm.bm[bq][lane] = __expf(ge[blk] - xs);
-            f32x4 a;
-            #pragma unroll
-            for (int M = 0; M < 4; ++M) a[M] = (M < blk) ? __expf(xs - ge[M]) : 0.0f;
-            *reinterpret_cast<f32x4*>(&sm.ai[bq][lane][0]) = a;
         }
     };
 
@@ -400,10 +413,13 @@ __device__ __forceinline__ void state_role(const ScanParams& p, Smem<DK, F32>& s
         }
     };
 
-    // step c: loads of c+4, staging of c+2, D_{c+1}; S_c out; S_{c+1} in
-    auto step = [&](int64_t c, int u, St& Rc, St& Rs, f32x4 (&Dn)[NDW], const f32x4 (&Dc)[NDW]) {
+    // step c: loads of c+4, staging of c+2 (the gate wave: tables of c+3,
+    // from the registers Rg loaded a step earlier), D_{c+1}; S_c out;
+    // S_{c+1} in
+    auto step = [&](int64_t c, int u, St& Rc, St& Rs, const St& Rg, f32x4 (&Dn)[NDW], const f32x4 (&Dc)[NDW]) {
         if constexpr (VW) prefetch(u & 1, c + PREFETCH);
         load_chunk(Rc, c + 4);
+        if (GW) gate_tables(Rg, (u + 3) & 3);
         stage(Rs, u & 1, (u + 2) & 3);
         fold_delta((u + 1) & 1, Dn);
         const bool live = c < x.n;
@@ -418,6 +434,7 @@ __device__ __forceinline__ void state_role(const ScanParams& p, Smem<DK, F32>& s
         // per-chunk arithmetic in straight line, one barrier.
         St R0;
         load_chunk(R0, 0);
+        if (GW) gate_tables(R0, 0);
         stage(R0, 0, 0);
         publish(0);
         lds_barrier();
@@ -435,6 +452,12 @@ __device__ __forceinline__ void state_role(const ScanParams& p, Smem<DK, F32>& s
     load_chunk(R1, 1);
     load_chunk(R2, 2);
     load_chunk(R3, 3);
+    if (GW) {  // tables and weights of chunks 0-2 (step c writes those of c + 3)
+        gate_tables(R0, 0);
+        gate_tables(R1, 1);
+        gate_tables(R2, 2);
+    }
+    lds_barrier();
     stage(R0, 0, 0);
     stage(R1, 1, 1);
     publish(0);
@@ -442,10 +465,10 @@ __device__ __forceinline__ void state_role(const ScanParams& p, Smem<DK, F32>& s
     fold_delta(0, D0);
     lds_barrier();
     for (int64_t c = 0; c < x.n; c += 4) {
-        step(c, 0, R0, R2, D1, D0);
-        step(c + 1, 1, R1, R3, D0, D1);
-        step(c + 2, 2, R2, R0, D1, D0);
-        step(c + 3, 3, R3, R1, D0, D1);
+        step(c, 0, R0, R2, R3, D1, D0);
+        step(c + 1, 1, R1, R3, R0, D0, D1);
+        step(c + 2, 2, R2, R0, R1, D1, D0);
+        step(c + 3, 3, R3, R1, R2, D0, D1);
     }
     store_final();
     if constexpr (VW) __asm__ volatile("" : : "v"(pf[0]), "v"(pf[1]));
@@ -645,6 +668,7 @@ __device__ __forceinline__ void output_role(const ScanParams& p, Smem<DK, F32>& 
     load_q(Q1, 1);
     load_q(Q2, 2);
     load_q(Q3, 3);
+    lds_barrier();  // the gate wave's first tables
     lds_barrier();
     q_operands(Q0, O0);
     scores(O0, 0, A0);

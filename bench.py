@@ -573,33 +573,43 @@ def main():
     del fp8, stage8, fp8_o, stage8_o, ref_stage, live8, other8
 
     # gated delta-rule layer (same shape as a linear-attention layer of the
-    # stack): one call = the (I + A)^-1 / score launch + the scan launch
-    ginp = synth.gdn_inputs(w.seed, 0, T, H, dk, dv, "bf16")
-    gd = {n: torch.from_numpy(ginp[n + "_dev"].view(np.int16)).view(torch.bfloat16).to(dev) for n in ("q", "k", "v")}
-    gd["g"] = torch.from_numpy(ginp["g"]).to(dev)
-    gd["beta"] = torch.from_numpy(ginp["beta"]).to(dev)
-    del ginp
-    g_o = torch.empty((T, H, dv), dtype=torch.float32, device=dev)
-    g_cs = torch.empty(((T + 63) // 64, H, dk, dv), dtype=torch.float32, device=dev)
-    g_fs = torch.empty((H, dk, dv), dtype=torch.float32, device=dev)
+    # stack): one call = the (I + A)^-1 launch + the scan launch.  Timed the
+    # way a stack runs its layers and the way the scan phases of the step are
+    # timed: back to back, two layers' inputs alternating, at the GPU's
+    # steady state under this load.  After an idle gap the per-call time of
+    # a back-to-back run first dips and then settles over ~40 calls (clock
+    # and power management: 0.59 ms, then up to 0.75 ms, then 0.55 ms), so
+    # 40 untimed calls come first.
+    gl = []
+    for l in range(2):
+        ginp = synth.gdn_inputs(w.seed, l, T, H, dk, dv, "bf16")
+        gd = {n: torch.from_numpy(ginp[n + "_dev"].view(np.int16)).view(torch.bfloat16).to(dev) for n in ("q", "k", "v")}
+        gd["g"] = torch.from_numpy(ginp["g"]).to(dev)
+        gd["beta"] = torch.from_numpy(ginp["beta"]).to(dev)
+        del ginp
+        gd["o"] = torch.empty((T, H, dv), dtype=torch.float32, device=dev)
+        gd["cs"] = torch.empty(((T + 63) // 64, H, dk, dv), dtype=torch.float32, device=dev)
+        gd["fs"] = torch.empty((H, dk, dv), dtype=torch.float32, device=dev)
+        gl.append(gd)
     g_ws = torch.empty(cap.gdn_workspace_bytes(T, H), dtype=torch.uint8, device=dev)
-    g_ms = []
+    n_gdn, w_gdn = 10, 40
+    g_ev = [torch.cuda.Event(enable_timing=True) for _ in range(n_gdn + 1)]
     with torch.cuda.stream(stream):
-        for rnd in range(5):
-            flush.fill_(rnd)
-            e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-            e[0].record(stream)
-            cap.gdn_chunked_prefill(gd["q"], gd["k"], gd["v"], gd["g"], gd["beta"], g_o, chunk_states=g_cs,
-                                    final_state=g_fs, workspace=g_ws, stream=stream)
-            e[1].record(stream)
-            stream.synchronize()
-            if rnd:
-                g_ms.append(e[0].elapsed_time(e[1]))
+        for rnd in range(n_gdn + w_gdn):
+            if rnd >= w_gdn:
+                g_ev[rnd - w_gdn].record(stream)
+            gd = gl[rnd % 2]
+            cap.gdn_chunked_prefill(gd["q"], gd["k"], gd["v"], gd["g"], gd["beta"], gd["o"], chunk_states=gd["cs"],
+                                    final_state=gd["fs"], workspace=g_ws, stream=stream)
+        g_ev[n_gdn].record(stream)
+    stream.synchronize()
+    g_ms = [g_ev[i].elapsed_time(g_ev[i + 1]) for i in range(n_gdn)]
+    g_o, g_cs, g_fs = gl[1]["o"], gl[1]["cs"], gl[1]["fs"]
     gdn_ms = float(np.median(g_ms))
     gdn_b = gdn_bytes(T, H, dk, dv)
     gdn_gbs = gdn_b / (gdn_ms * 1e-3) / 1e9
     assert bool(torch.isfinite(g_o).all()) and bool(torch.isfinite(g_fs).all())
-    del gd, g_o, g_cs, g_fs
+    del gd, gl, g_o, g_cs, g_fs
 
     # ---- robot episode reset (the gather verb), outside the timed step: 32
     # environments, a gallery of 8 capsules (18 KV layers [816 tokens, 1 head,

@@ -16,8 +16,9 @@
 //
 // Two launches.
 //  1. gdn_prepare, one wave per (chunk, head), all chunks in parallel: A from
-//     K K^T on MFMA and T = (I + A)^-1 by forward substitution in fp32 (lane
-//     j owns column j), written to the workspace as ready MFMA operands.  T
+//     K K^T on MFMA and T = (I + A)^-1 blockwise in fp32 (the four 16 x 16
+//     diagonal blocks by forward substitution, the blocks below them as
+//     fp32 MFMA products), written to the workspace as ready MFMA operands.  T
 //     depends on the chunk's inputs only -- not on S -- and is the same for
 //     every value slice of the head, so it is computed once, off the
 //     sequential path.
@@ -136,37 +137,84 @@ __global__ __launch_bounds__(64) void gdn_prepare_kernel(const GdnParams p) {
     uint8_t* rec = p.ws + (c * H + h) * kGdnWsRecord;
     __syncthreads();
 
-    // column `lane` of T: x_t = [t == lane] - sum_{m<t} A_tm x_m, applied
-    // column by column of A (x_m is final once every earlier column is in)
-    float xv[CH];
-    #pragma unroll
-    for (int t = 0; t < CH; ++t) xv[t] = (t == lane) ? 1.0f : 0.0f;
-    #pragma unroll
-    for (int m = 0; m < CH - 1; ++m) {
-        const float xm = xv[m];
+    // T = (I + A)^-1 by 16-row blocks.  `at` holds A^T above its diagonal
+    // (at[m][t] = A[t][m], t > m); T is stored row-major on and below the
+    // diagonal (at[t][m] = T[t][m], t >= m), so both live in one buffer.  T
+    // is lower triangular: its entries above the diagonal are never stored
+    // and every read of T masks them to zero.
+    //  1. T_ii = (I + A_ii)^-1 for the four diagonal blocks by forward
+    //     substitution in fp32, lane 16 i + j holding column j of block i;
+    //  2. T_ij = -T_ii (sum_{k=j}^{i-1} A_ik T_kj) for i > j, one block
+    //     diagonal d = i - j after the other, on v_mfma_f32_16x16x4_f32 (lane
+    //     l feeds A[l % 16][l / 16] and B[l / 16][l % 16] and receives
+    //     D[4 (l / 16) + r][l % 16]; fp32 products and sums).
+    auto tval = [&](int row, int col) -> float { return col <= row ? at[row * ATP + col] : 0.0f; };
+    {
+        const int bi = grp, j = li;
+        float x[16];
         #pragma unroll
-        for (int t4 = (m + 1) / 4; t4 < CH / 4; ++t4) {
-            const f32x4 a = *reinterpret_cast<const f32x4*>(&at[m * ATP + 4 * t4]);
+        for (int t = 0; t < 16; ++t) x[t] = (t == j) ? 1.0f : 0.0f;
+        #pragma unroll
+        for (int m = 0; m < 15; ++m) {
+            const float xm = x[m];
             #pragma unroll
-            for (int e = 0; e < 4; ++e)
-                if (4 * t4 + e > m) xv[4 * t4 + e] = fmaf(-a[e], xm, xv[4 * t4 + e]);
+            for (int t4 = (m + 1) / 4; t4 < 4; ++t4) {
+                const f32x4 a = *reinterpret_cast<const f32x4*>(&at[(16 * bi + m) * ATP + 16 * bi + 4 * t4]);
+                #pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (4 * t4 + e > m) x[4 * t4 + e] = fmaf(-a[e], xm, x[4 * t4 + e]);
+            }
         }
+        #pragma unroll
+        for (int t = 0; t < 16; ++t)
+            if (t >= j) at[(16 * bi + t) * ATP + 16 * bi + j] = x[t];
     }
-    // T row-major through LDS (the A^T rows are no longer needed), then the
-    // causal blocks in operand order, split hi/lo
     __syncthreads();
     #pragma unroll
-    for (int t = 0; t < CH; ++t) at[t * ATP + lane] = xv[t];
-    __syncthreads();
+    for (int d = 1; d < 4; ++d) {
+        // M_ij = sum_k A_ik T_kj, parked in T_ij's own place
+        #pragma unroll
+        for (int bj = 0; bj + d < 4; ++bj) {
+            const int bi = bj + d;
+            f32x4 m4 = {0.f, 0.f, 0.f, 0.f};
+            #pragma unroll
+            for (int k = bj; k < bi; ++k)
+                #pragma unroll
+                for (int s4 = 0; s4 < 4; ++s4) {
+                    const int sx = 16 * k + 4 * s4 + grp;
+                    m4 = __builtin_amdgcn_mfma_f32_16x16x4f32(at[sx * ATP + 16 * bi + li], tval(sx, 16 * bj + li), m4, 0,
+                                                             0, 0);
+                }
+            #pragma unroll
+            for (int r = 0; r < 4; ++r) at[(16 * bi + 4 * grp + r) * ATP + 16 * bj + li] = m4[r];
+        }
+        __syncthreads();
+        // T_ij = -T_ii M_ij over M_ij (each lane's stores follow its reads)
+        #pragma unroll
+        for (int bj = 0; bj + d < 4; ++bj) {
+            const int bi = bj + d;
+            f32x4 t4 = {0.f, 0.f, 0.f, 0.f};
+            #pragma unroll
+            for (int s4 = 0; s4 < 4; ++s4) {
+                const int sx = 4 * s4 + grp;
+                t4 = __builtin_amdgcn_mfma_f32_16x16x4f32(tval(16 * bi + li, 16 * bi + sx),
+                                                         at[(16 * bi + sx) * ATP + 16 * bj + li], t4, 0, 0, 0);
+            }
+            #pragma unroll
+            for (int r = 0; r < 4; ++r) at[(16 * bi + 4 * grp + r) * ATP + 16 * bj + li] = -t4[r];
+        }
+        __syncthreads();
+    }
+    // the causal blocks of T in operand order, split hi/lo
     #pragma unroll
     for (int r = 0; r < 4; ++r)
         #pragma unroll
         for (int i = 0; i <= r / 2; ++i) {
             const int blk = r < 2 ? r : 2 * r - 2 + i;
-            const float* src = &at[(16 * r + li) * ATP + 32 * i + 8 * grp];
-            const f32x4 a0 = *reinterpret_cast<const f32x4*>(src);
-            const f32x4 a1 = *reinterpret_cast<const f32x4*>(src + 4);
-            const float f[8] = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
+            const int row = 16 * r + li, col = 32 * i + 8 * grp;
+            float f[8];
+            #pragma unroll
+            for (int e = 0; e < 8; ++e) f[e] = tval(row, col + e);
             bf16x8 hi, lo;
             split_n<8>(f, hi, lo);
             *reinterpret_cast<bf16x8*>(rec + blk * 2048 + 16 * lane) = hi;

@@ -36,7 +36,10 @@ After the timed steps, outside them:
   * `cpu_baseline*`: the oracle on the host (see cpu_baseline).
 
 The JSON line's `value` is the capsule restore bandwidth (GB/s, bytes read +
-written); the scan and TTFT figures ride along as extra keys.  `roofline`
+written); the scan and TTFT figures ride along as extra keys.  The scan's MFMA
+figures: `scan_pct_mfma_useful` (useful flops / time / peak), its ceiling at
+full HBM bandwidth, and `scan_pct_mfma_busy_counter`, the MFMA pipe's busy
+fraction from rocprofv3 counters of the same kernel source.  `roofline`
 covers the dominant kernel (the scan, phase 1); `roofline_copy`,
 `roofline_snapshot` and `roofline_fork` the capsule copies, `gdn` and
 `gather` carry their own.
@@ -57,36 +60,49 @@ MFMA_BF16_PEAK_TFS = 2500.0  # MI355X dense bf16 MFMA, TFLOP/s
 LINK_PEAK_GBS = 64.0         # host link, PCIe 5.0 x16, one direction
 
 # HBM bytes per launch from rocprofv3 FETCH_SIZE / WRITE_SIZE runs (FETCH_SIZE
-# scaled by 1.99954 from a plain copy of known size); the counters belong to
-# the kernel source with the given sha256 and are reported only while it is
-# unchanged.  Summary and commands: profiles/hybrid48_hbm_traffic.md.
+# scaled by 1.99890 from the runtime's plain copies of known size); the
+# counters belong to the kernel source with the given sha256 and are reported
+# only while it is unchanged.  Summary and commands:
+# profiles/hybrid48_hbm_traffic.md.
+LINATTN_SRC = "paper_2606_20537_amd/csrc/linattn_scan.hip"
+COPY_SRC = "paper_2606_20537_amd/csrc/capsule_copy.hip"
+GDN_SRC = "paper_2606_20537_amd/csrc/gdn_scan.hip"
+LINATTN_SHA = "5ace4d0fe56b9677f56c665ff31aaa5b01b6b4934210ca1cecd5edc64df1ea2d"
+COPY_SHA = "3fe58e0a55a7b15d596057bce3dc33d9409338b3d9d5d137fddb7f8da5978430"
+GDN_SHA = "db0622c485bad0e0ff8e0d479e10badb1f34ecad3c439a60cbb70ebcfe336a30"
 MEASURED_TRAFFIC = {
-    "scan_cs": {"src": "paper_2606_20537_amd/csrc/linattn_scan.hip",
-                "sha256": "162440648dff978016a93b9f6e267fc00fad03f344b672ae799c6c1d6802d591",
-                "bytes": 1227813135},
-    "restore": {"src": "paper_2606_20537_amd/csrc/capsule_copy.hip",
-                "sha256": "7c114eda4a9bfbb8004abca49d610710b02b7f73425ed97266d767f35e4ffc66",
-                "bytes": 1763895780},
-    "snapshot": {"src": "paper_2606_20537_amd/csrc/capsule_copy.hip",
-                 "sha256": "7c114eda4a9bfbb8004abca49d610710b02b7f73425ed97266d767f35e4ffc66",
-                 "bytes": 1763952498},
-    "fork4": {"src": "paper_2606_20537_amd/csrc/capsule_copy.hip",
-              "sha256": "7c114eda4a9bfbb8004abca49d610710b02b7f73425ed97266d767f35e4ffc66",
-              "bytes": 4410198017},
-    "gather": {"src": "paper_2606_20537_amd/csrc/capsule_copy.hip",
-               "sha256": "7c114eda4a9bfbb8004abca49d610710b02b7f73425ed97266d767f35e4ffc66",
-               "bytes": 1063125363},
-    "gdn": {"src": "paper_2606_20537_amd/csrc/gdn_scan.hip",
-            "sha256": "7793817bb93174accbb7982128d2d941343977fe70c772fbe1f90a1cae78e346",
-            "bytes": 1619575466},
+    "scan_cs": {"src": LINATTN_SRC, "sha256": LINATTN_SHA, "bytes": 1228393946},
+    "restore": {"src": COPY_SRC, "sha256": COPY_SHA, "bytes": 1763614123},
+    "snapshot": {"src": COPY_SRC, "sha256": COPY_SHA, "bytes": 1763736054},
+    "fork4": {"src": COPY_SRC, "sha256": COPY_SHA, "bytes": 4409925167},
+    "gather": {"src": COPY_SRC, "sha256": COPY_SHA, "bytes": 1008475201},
+    "gdn": {"src": GDN_SRC, "sha256": GDN_SHA, "bytes": 1622764826},
+}
+
+# MFMA pipe busy from SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x GRBM_GUI_ACTIVE
+# / 8 XCDs), per scan launch on the 48-layer workload, with the same sha256
+# guard.  Summary and commands: profiles/hybrid48_scan_counters.md.
+MEASURED_MFMA_BUSY = {
+    "scan_cs": {"src": LINATTN_SRC, "sha256": LINATTN_SHA, "frac": 0.1541},
+    "scan_final": {"src": LINATTN_SRC, "sha256": LINATTN_SHA, "frac": 0.1769},
+    "gdn_scan": {"src": GDN_SRC, "sha256": GDN_SHA, "frac": 0.1628},
 }
 
 
-def measured_traffic(key):
+def _src_unchanged(m):
     import hashlib
-    m = MEASURED_TRAFFIC[key]
     with open(os.path.join(ROOT, m["src"]), "rb") as f:
-        return m["bytes"] if hashlib.sha256(f.read()).hexdigest() == m["sha256"] else None
+        return hashlib.sha256(f.read()).hexdigest() == m["sha256"]
+
+
+def measured_traffic(key):
+    m = MEASURED_TRAFFIC[key]
+    return m["bytes"] if _src_unchanged(m) else None
+
+
+def measured_mfma_busy(key):
+    m = MEASURED_MFMA_BUSY[key]
+    return round(100 * m["frac"], 2) if _src_unchanged(m) else None
 
 
 def parse():
@@ -796,6 +812,13 @@ def main():
         "scan_tokens_per_s": round(T / (ms["scan_cs"] * 1e-3), 1),
         "scan_tokens_per_s_final_only": round(T / (ms["scan_final"] * 1e-3), 1),
         "scan_pct_mfma_useful": round(100 * flops / (scan_launch_ms * 1e-3) / (MFMA_BF16_PEAK_TFS * 1e12), 3),
+        "scan_pct_mfma_useful_ceiling": round(100 * flops / (scan_b / (HBM_PEAK_GBS * 1e9)) / (MFMA_BF16_PEAK_TFS * 1e12), 2),
+        "scan_pct_mfma_busy_counter": {"chunk_states": measured_mfma_busy("scan_cs"),
+                                       "final_only": measured_mfma_busy("scan_final"),
+                                       "gdn_scan": measured_mfma_busy("gdn_scan"),
+                                       "what": "MFMA pipe busy cycles / SIMD cycles (rocprofv3 counters, "
+                                               "profiles/hybrid48_scan_counters.md); executed products include "
+                                               "the hi/lo operand terms and the recomputed scores"},
         "ttft_ms": {"cold": percentiles(ttft["cold"]), "capsule": percentiles(ttft["capsule"]),
                     "restore_over_cold_ratio_p50": round(float(np.percentile(ttft["cold"], 50))
                                                          / float(np.percentile(ttft["capsule"], 50)), 3),

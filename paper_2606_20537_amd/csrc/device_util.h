@@ -72,13 +72,24 @@ __device__ inline float lane_value(float x, int l) {
 // hi + lo carries ~16 significant bits, so a product of split operands
 // (three MFMA terms, or two when one side is exact bf16) keeps ~2^-17
 // relative error.
+// Values go in pairs: one packed conversion gives both hi halves, which are
+// widened back to fp32 with a shift and a mask (no second conversion).
 template <int N, typename V>
 __device__ inline void split_n(const float* f, V& hi, V& lo) {
+    static_assert(N % 2 == 0, "pairs");
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
     #pragma unroll
-    for (int e = 0; e < N; ++e) {
-        const __bf16 h = (__bf16)f[e];
-        hi[e] = h;
-        lo[e] = (__bf16)(f[e] - (float)h);
+    for (int e = 0; e < N; e += 2) {
+        const bf16x2 h = __builtin_convertvector((f32x2){f[e], f[e + 1]}, bf16x2);
+        const uint32_t u = __builtin_bit_cast(uint32_t, h);
+        const float h0 = __builtin_bit_cast(float, u << 16);
+        const float h1 = __builtin_bit_cast(float, u & 0xFFFF0000u);
+        const bf16x2 l = __builtin_convertvector((f32x2){f[e] - h0, f[e + 1] - h1}, bf16x2);
+        hi[e] = h[0];
+        hi[e + 1] = h[1];
+        lo[e] = l[0];
+        lo[e + 1] = l[1];
     }
 }
 

@@ -264,7 +264,7 @@ CAP_API uint64_t capsule_digest_tokens(const int32_t* ids, uint64_t n);
  * Supported: chunk == 64, dk in {64, 128} (fp32 inputs: dk == 64), dv a
  * multiple of 16, 1 <= H, H dk dv 4 < 2^31 and 64 H max(dk, dv) 4 < 2^31
  * (32-bit offsets inside one state and one chunk),
- * 0 <= T; pointers 16-byte aligned; o / chunk_states / final_state must not
+ * 0 <= T <= 2^36; pointers 16-byte aligned; o / chunk_states / final_state must not
  * overlap the inputs (except final_state == state_in).
  * Errors: CAP_E_INVAL (null required pointer, T < 0, H < 1, bad dtype,
  * overlap), CAP_E_UNSUPPORTED (shape outside the list), CAP_E_ALIGN. */

@@ -858,12 +858,13 @@ int validate_linattn(const linattn_args* a, ScanParams* out) {
     if (a->in_dtype == CAP_DTYPE_F32 && a->dk != 64) return CAP_E_UNSUPPORTED;
     if ((int64_t)a->H * (a->dv / 16) > 0x7fffffff) return CAP_E_UNSUPPORTED;
     // the kernels address one chunk of rows, and one state of all heads, with
-    // 32-bit byte offsets
+    // 32-bit byte offsets, and count chunks in 32 bits
     {
         const uint64_t H = (uint64_t)a->H, dk = (uint64_t)a->dk, dv = (uint64_t)a->dv;
         if (64 * H * (dk > dv ? dk : dv) * 4 > 0x7fffffffull || H * dk * dv * 4 > 0x7fffffffull)
             return CAP_E_UNSUPPORTED;
     }
+    if (a->T > ((int64_t)1 << 36)) return CAP_E_UNSUPPORTED;
     if (a->T > 0 && (!a->q || !a->k || !a->v || !a->g || !a->o)) return CAP_E_INVAL;
     const uint64_t ptrs[] = {(uint64_t)(uintptr_t)a->q, (uint64_t)(uintptr_t)a->k, (uint64_t)(uintptr_t)a->v,
                              (uint64_t)(uintptr_t)a->g, (uint64_t)(uintptr_t)a->state_in,

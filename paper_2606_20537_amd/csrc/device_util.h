@@ -32,6 +32,13 @@ __device__ inline rsrc_t make_rsrc(const void* base, int64_t nbytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, 0x00020000);
 }
 
+// Buffer resource over [base, base + nbytes) for an nbytes the caller knows
+// to be below 2^31 (no clamp: with wave-uniform arguments it is built on the
+// scalar unit).
+__device__ inline rsrc_t make_rsrc_u32(const void* base, uint32_t nbytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)nbytes, 0x00020000);
+}
+
 // Transposing LDS read of a row-major bf16 tile with `pitch` elements per
 // row: lane n of each 16-lane group gets tile[k0 + 0..3][n0 + n].  k0 may
 // differ between the four groups of a wave.

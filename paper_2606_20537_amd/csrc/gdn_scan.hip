@@ -246,9 +246,18 @@ struct alignas(16) GdnSmem {
 
 struct GdnCtx {
     int h, j0, H, dv, lane, li, grp;
+    int nfull, tail;               // full chunks, rows of the partial last one
     int64_t T, n;                  // tokens, chunks
     int64_t qk_row, v_row, o_row;  // bytes per token of q / k, v, o
 };
+
+// Valid rows of chunk c: CH up to the last full chunk, then the tail, then 0
+// (chunks past the end), in 32-bit arithmetic (the host bounds the chunk
+// count below 2^31 and a chunk's bytes of any tensor below 2^31).
+__device__ inline uint32_t chunk_rows(const GdnCtx& x, int64_t c) {
+    const int ci = (int)c;
+    return ci < x.nfull ? (uint32_t)CH : (ci == x.nfull ? (uint32_t)x.tail : 0u);
+}
 
 // Every product is computed transposed, with the value column j as the row
 // index of the accumulator: lane (grp, li) then holds four consecutive
@@ -294,15 +303,16 @@ __device__ __forceinline__ void out_role(const GdnParams& p, GdnSmem<DK>& sm, co
     const int ot = 64 * R + lane;
 
     auto load = [&](St& S_, int64_t c) {
-        const int64_t t0 = c * CH, rows = x.T - t0;
-        const rsrc_t rk = make_rsrc(static_cast<const char*>(p.k) + t0 * x.qk_row, rows * x.qk_row);
+        const int64_t t0 = c * CH;
+        const uint32_t rows = chunk_rows(x, c);
+        const rsrc_t rk = make_rsrc_u32(static_cast<const char*>(p.k) + t0 * x.qk_row, rows * (uint32_t)x.qk_row);
         #pragma unroll
         for (int u = 0; u < PK; ++u) {
             const int pc = ot + NO_T * u;
             const int m = pc / (DK / 8), d0 = (pc % (DK / 8)) * 8;
             S_.kp[u] = __builtin_amdgcn_raw_buffer_load_b128(rk, (uint32_t)(m * x.qk_row + ((int64_t)h * DK + d0) * 2), 0, 0);
         }
-        const rsrc_t rq = make_rsrc(static_cast<const char*>(p.q) + t0 * x.qk_row, rows * x.qk_row);
+        const rsrc_t rq = make_rsrc_u32(static_cast<const char*>(p.q) + t0 * x.qk_row, rows * (uint32_t)x.qk_row);
         #pragma unroll
         for (int kk = 0; kk < NKK; ++kk)
             S_.q[kk] = __builtin_amdgcn_raw_buffer_load_b128(
@@ -310,7 +320,7 @@ __device__ __forceinline__ void out_role(const GdnParams& p, GdnSmem<DK>& sm, co
         const bool live = c < x.n;
         const uint8_t* rec = p.ws + (live ? (c * H + h) * kGdnWsRecord : 0);
         if constexpr (R == 0) {
-            const rsrc_t rt = make_rsrc(rec + kGdnWsTabOff, live ? 2 * CH * 4 : 0);
+            const rsrc_t rt = make_rsrc_u32(rec + kGdnWsTabOff, live ? 2u * CH * 4 : 0u);
             const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(rt, (uint32_t)(8 * lane), 0, 0);
             const uint32_t v0 = v[0], v1 = v[1];
             S_.tab[0] = f32_of(v0);
@@ -345,7 +355,8 @@ __device__ __forceinline__ void out_role(const GdnParams& p, GdnSmem<DK>& sm, co
     uint32_t pf[4] = {0u, 0u, 0u, 0u};
     auto prefetch = [&](int slot, int64_t c) {
         __asm__ volatile("" : : "v"(pf[slot]));
-        const int64_t t0 = c * CH, rows = x.T - t0;
+        const int64_t t0 = c * CH;
+        const int rows = (int)chunk_rows(x, c);
         const int ns = dv / DVS;
         const int L = j0 / DVS + ns * (64 * (R - 1) + lane);
         constexpr int LK = DK * 2 / 128;            // 128-byte lines per row of K or Q
@@ -371,7 +382,7 @@ __device__ __forceinline__ void out_role(const GdnParams& p, GdnSmem<DK>& sm, co
         const bool live = c < x.n;
         const int b = (int)(c & 1);
         const __bf16* kb = sm.k[b];
-        const int64_t t0 = c * CH, rows = x.T - t0;
+        const int64_t t0 = c * CH;
         if constexpr (!ONE) load(ld, c + 3);
         if constexpr (!ONE && (R == 1 || R == 2)) prefetch(slot, c + PREFETCH);
 
@@ -446,7 +457,8 @@ __device__ __forceinline__ void out_role(const GdnParams& p, GdnSmem<DK>& sm, co
             oa = mma(ul, ph[i2], oa);
             oa = mma(uh, pl[i2], oa);
         }
-        const rsrc_t ro = make_rsrc(static_cast<char*>(static_cast<void*>(p.o)) + t0 * x.o_row, rows * x.o_row);
+        const rsrc_t ro = make_rsrc_u32(static_cast<char*>(static_cast<void*>(p.o)) + t0 * x.o_row,
+                                        chunk_rows(x, c) * (uint32_t)x.o_row);
         f32x4 os;
         #pragma unroll
         for (int q = 0; q < 4; ++q) os[q] = oa[q] * p.scale;
@@ -509,12 +521,14 @@ __device__ __forceinline__ void chain_role(const GdnParams& p, GdnSmem<DK>& sm, 
         S[u] = p.state_in ? *reinterpret_cast<const f32x4*>(p.state_in + srow(u)) : f32x4{0.f, 0.f, 0.f, 0.f};
 
     auto load = [&](St& S_, int64_t c) {
-        const int64_t t0 = c * CH, rows = x.T - t0;
-        const rsrc_t rv = make_rsrc(static_cast<const char*>(p.v) + t0 * x.v_row, rows * x.v_row);
+        const int64_t t0 = c * CH;
+        const rsrc_t rv = make_rsrc_u32(static_cast<const char*>(p.v) + t0 * x.v_row,
+                                        chunk_rows(x, c) * (uint32_t)x.v_row);
         S_.v = __builtin_amdgcn_raw_buffer_load_b64(
             rv, (uint32_t)((16 * R + li) * x.v_row + ((int64_t)h * dv + j0 + 4 * grp) * 2), 0, 0);
         const bool live = c < x.n;
-        const rsrc_t rt = make_rsrc(p.ws + (live ? (c * H + h) * kGdnWsRecord : 0), live ? kGdnWsTBytes : 0);
+        const rsrc_t rt = make_rsrc_u32(p.ws + (live ? (c * H + h) * kGdnWsRecord : 0),
+                                        live ? (uint32_t)kGdnWsTBytes : 0u);
         #pragma unroll
         for (int i = 0; i < NT2; ++i) {
             const int blk = R < 2 ? R : 2 * R - 2 + i;
@@ -622,8 +636,8 @@ __device__ __forceinline__ void chain_role(const GdnParams& p, GdnSmem<DK>& sm, 
         if (live) lds_barrier();
 
         // ---- phase 3: S_c to chunk_states[c]; S^T <- gamma_last S^T + (w U)^T K
-        const rsrc_t rc = make_rsrc(p.chunk_states + (live ? c : 0) * state_elems,
-                                    live && p.chunk_states ? state_elems * 4 : 0);
+        const rsrc_t rc = make_rsrc_u32(p.chunk_states + (live ? c : 0) * state_elems,
+                                        live && p.chunk_states ? (uint32_t)(state_elems * 4) : 0u);
         #pragma unroll
         for (int u = 0; u < NDW; ++u)
             __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, S[u]), rc, (uint32_t)(srow(u) * 4), 0, 0);
@@ -692,6 +706,8 @@ __global__ __launch_bounds__(NT) void gdn_scan_kernel(const GdnParams p) {
     x.grp = x.lane >> 4;
     x.T = p.T;
     x.n = (p.T + CH - 1) / CH;
+    x.nfull = (int)(p.T / CH);
+    x.tail = (int)(p.T % CH);
     x.qk_row = (int64_t)x.H * DK * 2;
     x.v_row = (int64_t)x.H * x.dv * 2;
     x.o_row = (int64_t)x.H * x.dv * 4;

@@ -171,9 +171,18 @@ struct QStage {
 // Per-workgroup constants shared by both roles.
 struct Ctx {
     int h, j0, H, dv, lane, li, grp;
+    int nfull, tail;               // full chunks, rows of the partial last one
     int64_t T, n;                  // tokens, chunks
     int64_t qk_row, v_row, o_row;  // bytes per token of q / k, v, o
 };
+
+// Valid rows of chunk c: CH up to the last full chunk, then the tail, then 0
+// (chunks past the end).  32-bit arithmetic: the host bounds the number of
+// chunks below 2^30, and a chunk's bytes of any tensor below 2^31.
+__device__ inline uint32_t chunk_rows(const Ctx& x, int64_t c) {
+    const int ci = (int)c;
+    return ci < x.nfull ? (uint32_t)CH : (ci == x.nfull ? (uint32_t)x.tail : 0u);
+}
 
 // Both roles walk the chunks four steps per loop iteration (the register
 // stages rotate without copies).  Every global access of a step is issued
@@ -228,8 +237,8 @@ __device__ __forceinline__ void state_role(const ScanParams& p, Smem<DK, F32>& s
 
     auto load_chunk = [&](St& R, int64_t c) {
         const int64_t t0 = c * CH;
-        const int64_t rows = x.T - t0;
-        const rsrc_t rk = make_rsrc(static_cast<const char*>(p.k) + t0 * x.qk_row, rows * x.qk_row);
+        const uint32_t rows = chunk_rows(x, c);
+        const rsrc_t rk = make_rsrc_u32(static_cast<const char*>(p.k) + t0 * x.qk_row, rows * (uint32_t)x.qk_row);
         #pragma unroll
         for (int u = 0; u < PK; ++u) {
             const int pc = st + NS_T * u;
@@ -240,7 +249,7 @@ __device__ __forceinline__ void state_role(const ScanParams& p, Smem<DK, F32>& s
         if constexpr (VW) {
             // V slice (lane l: rows l/2 and 32 + l/2, columns 8 (l%2)..+7),
             // loaded by one wave only, so no two waves wait on the same lines
-            const rsrc_t rv = make_rsrc(static_cast<const char*>(p.v) + t0 * x.v_row, rows * x.v_row);
+            const rsrc_t rv = make_rsrc_u32(static_cast<const char*>(p.v) + t0 * x.v_row, rows * (uint32_t)x.v_row);
             #pragma unroll
             for (int i = 0; i < 2; ++i)
                 load_piece<F32>(R.vp[i], rv, (uint32_t)(((lane >> 1) + 32 * i) * x.v_row +
@@ -249,7 +258,7 @@ __device__ __forceinline__ void state_role(const ScanParams& p, Smem<DK, F32>& s
         if ((VW && ONE) || GW) {
             // the log-gates (lane t: token t): the gate wave's, and the V
             // wave's in a call of at most one chunk
-            const rsrc_t rg = make_rsrc(p.g + t0 * H, rows * H * 4);
+            const rsrc_t rg = make_rsrc_u32(p.g + t0 * H, rows * (uint32_t)(H * 4));
             R.g = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rg, (uint32_t)((lane * H + h) * 4), 0, 0));
         }
     };
@@ -368,22 +377,23 @@ __device__ __forceinline__ void state_role(const ScanParams& p, Smem<DK, F32>& s
     auto prefetch = [&](int slot, int64_t c) {
         __asm__ volatile("" : : "v"(pf[slot]));
         const int64_t t0 = c * CH;
-        const int64_t rows = x.T - t0;
+        const uint32_t rows = chunk_rows(x, c);
         const int s8 = (j0 / DVS) & 7;
         const int tsel = lane >> 4, i = lane & 15;
         const uint32_t qoff = (uint32_t)((8 * s8 + (i >> 1)) * x.qk_row + (int64_t)h * DK * ES + (i & 1) * 128);
         const uint32_t voff = (uint32_t)((16 * (s8 & 3) + i) * x.v_row + (int64_t)h * dv * ES + (s8 >> 2) * 128);
         const int64_t row_b = tsel == 2 ? x.v_row : x.qk_row;
         const void* base = tsel == 0 ? p.q : tsel == 1 ? p.k : p.v;
-        const rsrc_t r = make_rsrc(static_cast<const char*>(base) + t0 * row_b, tsel == 3 ? 0 : rows * row_b);
+        const rsrc_t r = make_rsrc_u32(static_cast<const char*>(base) + t0 * row_b,
+                                       tsel == 3 ? 0u : rows * (uint32_t)row_b);
         pf[slot] = __builtin_amdgcn_raw_buffer_load_b32(r, tsel == 2 ? voff : qoff, 0, 0);
     };
 
     // S_c as chunk state c (an empty buffer range when not wanted)
     auto store_state = [&](int64_t c, bool live) {
         const bool on = live && p.chunk_states != nullptr;
-        const rsrc_t rc = make_rsrc(p.chunk_states + (on ? c * (int64_t)H * DK * dv : 0),
-                                    on ? (int64_t)H * DK * dv * 4 : 0);
+        const rsrc_t rc = make_rsrc_u32(p.chunk_states + (on ? c * (int64_t)H * DK * dv : 0),
+                                        on ? (uint32_t)(H * DK * dv * 4) : 0u);
         #pragma unroll
         for (int t = 0; t < NDW; ++t) {
             #pragma unroll
@@ -500,7 +510,8 @@ __device__ __forceinline__ void output_role(const ScanParams& p, Smem<DK, F32>& 
     // piece l % PPR of row RPI i + l / PPR
     auto load_q = [&](QS& Q, int64_t c) {
         const int64_t t0 = c * CH;
-        const rsrc_t rq = make_rsrc(static_cast<const char*>(p.q) + t0 * x.qk_row, (x.T - t0) * x.qk_row);
+        const rsrc_t rq = make_rsrc_u32(static_cast<const char*>(p.q) + t0 * x.qk_row,
+                                        chunk_rows(x, c) * (uint32_t)x.qk_row);
         #pragma unroll
         for (int i = 0; i < NQI; ++i)
             Q.qp[i] = __builtin_amdgcn_raw_buffer_load_b128(
@@ -628,7 +639,8 @@ __device__ __forceinline__ void output_role(const ScanParams& p, Smem<DK, F32>& 
         // the chunk's buffer range and are dropped
         {
             const int64_t t0 = c * CH;
-            const rsrc_t ro = make_rsrc(reinterpret_cast<const char*>(p.o) + t0 * x.o_row, (x.T - t0) * x.o_row);
+            const rsrc_t ro = make_rsrc_u32(reinterpret_cast<const char*>(p.o) + t0 * x.o_row,
+                                            chunk_rows(x, c) * (uint32_t)x.o_row);
             const f32x4 eg = *reinterpret_cast<const f32x4*>(&sm.eG[u][16 * W + 4 * grp]);
             #pragma unroll
             for (int r = 0; r < 4; ++r) {
@@ -705,6 +717,8 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
     x.grp = x.lane >> 4;
     x.T = p.T;
     x.n = (p.T + CH - 1) / CH;
+    x.nfull = (int)(p.T / CH);
+    x.tail = (int)(p.T % CH);
     constexpr int ES = F32 ? 4 : 2;
     x.qk_row = (int64_t)x.H * DK * ES;
     x.v_row = (int64_t)x.H * x.dv * ES;

@@ -167,6 +167,8 @@ def test_scan_argument_checks():
     # more heads than 32-bit offsets inside one state of all heads can address
     assert _scan_status(H=32768, dk=128, dv=128) == cap.CAP_E_UNSUPPORTED
     assert _scan_status(H=32767, dk=128, dv=128, T=0, q=0, k=0, v=0, g=0, o=0) == cap.CAP_OK
+    # more chunks than the kernels count in 32 bits
+    assert _scan_status(T=(1 << 36) + 1) == cap.CAP_E_UNSUPPORTED
 
 
 def test_decode_step_argument_checks():

@@ -67,25 +67,25 @@ LINK_PEAK_GBS = 64.0         # host link, PCIe 5.0 x16, one direction
 LINATTN_SRC = "paper_2606_20537_amd/csrc/linattn_scan.hip"
 COPY_SRC = "paper_2606_20537_amd/csrc/capsule_copy.hip"
 GDN_SRC = "paper_2606_20537_amd/csrc/gdn_scan.hip"
-LINATTN_SHA = "5ace4d0fe56b9677f56c665ff31aaa5b01b6b4934210ca1cecd5edc64df1ea2d"
+LINATTN_SHA = "9643aa1bd5851b4567d8a8cb75b2478d3cd82f4c4fd4f9b466160fd423b7031f"
 COPY_SHA = "3fe58e0a55a7b15d596057bce3dc33d9409338b3d9d5d137fddb7f8da5978430"
-GDN_SHA = "db0622c485bad0e0ff8e0d479e10badb1f34ecad3c439a60cbb70ebcfe336a30"
+GDN_SHA = "dc61627aa63d9cce1b879f5ad40129a17c475eaff73c61d2623edb178a540b9d"
 MEASURED_TRAFFIC = {
-    "scan_cs": {"src": LINATTN_SRC, "sha256": LINATTN_SHA, "bytes": 1228393946},
-    "restore": {"src": COPY_SRC, "sha256": COPY_SHA, "bytes": 1763614123},
-    "snapshot": {"src": COPY_SRC, "sha256": COPY_SHA, "bytes": 1763736054},
-    "fork4": {"src": COPY_SRC, "sha256": COPY_SHA, "bytes": 4409925167},
-    "gather": {"src": COPY_SRC, "sha256": COPY_SHA, "bytes": 1008475201},
-    "gdn": {"src": GDN_SRC, "sha256": GDN_SHA, "bytes": 1622764826},
+    "scan_cs": {"src": LINATTN_SRC, "sha256": LINATTN_SHA, "bytes": 1229000834},
+    "restore": {"src": COPY_SRC, "sha256": COPY_SHA, "bytes": 1763610641},
+    "snapshot": {"src": COPY_SRC, "sha256": COPY_SHA, "bytes": 1763695298},
+    "fork4": {"src": COPY_SRC, "sha256": COPY_SHA, "bytes": 4409891280},
+    "gather": {"src": COPY_SRC, "sha256": COPY_SHA, "bytes": 1009687365},
+    "gdn": {"src": GDN_SRC, "sha256": GDN_SHA, "bytes": 1620970101},
 }
 
 # MFMA pipe busy from SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x GRBM_GUI_ACTIVE
 # / 8 XCDs), per scan launch on the 48-layer workload, with the same sha256
 # guard.  Summary and commands: profiles/hybrid48_scan_counters.md.
 MEASURED_MFMA_BUSY = {
-    "scan_cs": {"src": LINATTN_SRC, "sha256": LINATTN_SHA, "frac": 0.1541},
-    "scan_final": {"src": LINATTN_SRC, "sha256": LINATTN_SHA, "frac": 0.1769},
-    "gdn_scan": {"src": GDN_SRC, "sha256": GDN_SHA, "frac": 0.1628},
+    "scan_cs": {"src": LINATTN_SRC, "sha256": LINATTN_SHA, "frac": 0.1560},
+    "scan_final": {"src": LINATTN_SRC, "sha256": LINATTN_SHA, "frac": 0.1854},
+    "gdn_scan": {"src": GDN_SRC, "sha256": GDN_SHA, "frac": 0.1659},
 }
 
 

@@ -242,6 +242,11 @@ struct alignas(16) GdnSmem {
     alignas(16) __bf16 u[2][CH * JP];     // U [m][j]: hi, lo
     alignas(16) __bf16 wu[2][CH * JP];    // w U [m][j], w_m = exp(G_last - G_m): hi, lo
     alignas(16) float tab[2][2 * CH];     // by chunk parity: G_m log2(e) (0..63), beta_m (64..127)
+    // decay factors of the scores below the diagonal blocks, by chunk
+    // parity: exp(G_e - G_m) with e the last token of m's 16-token block,
+    // and exp(G_i - G_e(M)) for the blocks M before i's (0 elsewhere)
+    alignas(16) float bm[2][CH];
+    alignas(16) float ai[2][CH][4];
 };
 
 struct GdnCtx {
@@ -339,6 +344,17 @@ __device__ __forceinline__ void out_role(const GdnParams& p, GdnSmem<DK>& sm, co
         if constexpr (R == 0) {
             sm.tab[bk][2 * lane] = S_.tab[0];
             sm.tab[bk][2 * lane + 1] = S_.tab[1];
+            // the factored decay (lane t: token t); both factors in (0, 1]
+            const float g = sm.tab[bk][lane];
+            const int blk = lane >> 4;
+            float ge[4];
+            #pragma unroll
+            for (int M = 0; M < 4; ++M) ge[M] = sm.tab[bk][16 * M + 15];
+            sm.bm[bk][lane] = exp2f(ge[blk] - g);
+            f32x4 a;
+            #pragma unroll
+            for (int M = 0; M < 4; ++M) a[M] = (M < blk) ? exp2f(g - ge[M]) : 0.0f;
+            *reinterpret_cast<f32x4*>(&sm.ai[bk][lane][0]) = a;
         }
     };
 
@@ -413,7 +429,10 @@ __device__ __forceinline__ void out_role(const GdnParams& p, GdnSmem<DK>& sm, co
         }
         // P^T = scores o exp(G_i - G_m) for m <= i, as the B operand of
         // U^T P^T: element e of step i2 is m = 32 i2 + 16 (e / 4) + 4 grp + e % 4
+        // below the diagonal block exp(G_i - G_m) = exp(G_i - G_e) exp(G_e - G_m)
+        // from the tables; on it exp2 of the difference, masked to m <= i
         const float g2i = sm.tab[b][16 * R + li];
+        const f32x4 aiv = *reinterpret_cast<const f32x4*>(&sm.ai[b][16 * R + li][0]);
         bf16x8 ph[NT2], pl[NT2];
         #pragma unroll
         for (int i2 = 0; i2 < NT2; ++i2) {
@@ -426,10 +445,16 @@ __device__ __forceinline__ void out_role(const GdnParams& p, GdnSmem<DK>& sm, co
                     for (int q = 0; q < 4; ++q) f[4 * half + q] = 0.0f;
                     continue;
                 }
-                const f32x4 gm = *reinterpret_cast<const f32x4*>(&sm.tab[b][16 * mb + 4 * grp]);
-                #pragma unroll
-                for (int q = 0; q < 4; ++q)
-                    f[4 * half + q] = (mb < R || 4 * grp + q <= li) ? sc[mb][q] * exp2f(g2i - gm[q]) : 0.0f;
+                if (mb < R) {
+                    const f32x4 bmv = *reinterpret_cast<const f32x4*>(&sm.bm[b][16 * mb + 4 * grp]);
+                    #pragma unroll
+                    for (int q = 0; q < 4; ++q) f[4 * half + q] = (sc[mb][q] * aiv[mb]) * bmv[q];
+                } else {
+                    const f32x4 gm = *reinterpret_cast<const f32x4*>(&sm.tab[b][16 * mb + 4 * grp]);
+                    #pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        f[4 * half + q] = (4 * grp + q <= li) ? sc[mb][q] * exp2f(g2i - gm[q]) : 0.0f;
+                }
             }
             split_n<8>(f, ph[i2], pl[i2]);
         }

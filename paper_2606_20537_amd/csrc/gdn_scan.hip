@@ -129,7 +129,7 @@ __global__ __launch_bounds__(64) void gdn_prepare_kernel(const GdnParams p) {
             f32x4 a;
             #pragma unroll
             for (int q = 0; q < 4; ++q)
-                a[q] = (16 * r + 4 * grp + q > m) ? bt[q] * exp2f(gt[q] - gm) * acc[q] : 0.0f;
+                a[q] = (16 * r + 4 * grp + q > m) ? bt[q] * __builtin_amdgcn_exp2f(gt[q] - gm) * acc[q] : 0.0f;
             *reinterpret_cast<f32x4*>(&at[m * ATP + 16 * r + 4 * grp]) = a;
         }
     }
@@ -350,10 +350,10 @@ __device__ __forceinline__ void out_role(const GdnParams& p, GdnSmem<DK>& sm, co
             float ge[4];
             #pragma unroll
             for (int M = 0; M < 4; ++M) ge[M] = sm.tab[bk][16 * M + 15];
-            sm.bm[bk][lane] = exp2f(ge[blk] - g);
+            sm.bm[bk][lane] = __builtin_amdgcn_exp2f(ge[blk] - g);
             f32x4 a;
             #pragma unroll
-            for (int M = 0; M < 4; ++M) a[M] = (M < blk) ? exp2f(g - ge[M]) : 0.0f;
+            for (int M = 0; M < 4; ++M) a[M] = (M < blk) ? __builtin_amdgcn_exp2f(g - ge[M]) : 0.0f;
             *reinterpret_cast<f32x4*>(&sm.ai[bk][lane][0]) = a;
         }
     };
@@ -453,14 +453,14 @@ __device__ __forceinline__ void out_role(const GdnParams& p, GdnSmem<DK>& sm, co
                     const f32x4 gm = *reinterpret_cast<const f32x4*>(&sm.tab[b][16 * mb + 4 * grp]);
                     #pragma unroll
                     for (int q = 0; q < 4; ++q)
-                        f[4 * half + q] = (4 * grp + q <= li) ? sc[mb][q] * exp2f(g2i - gm[q]) : 0.0f;
+                        f[4 * half + q] = (4 * grp + q <= li) ? sc[mb][q] * __builtin_amdgcn_exp2f(g2i - gm[q]) : 0.0f;
                 }
             }
             split_n<8>(f, ph[i2], pl[i2]);
         }
         f32x4 oa;
         {
-            const float gam = exp2f(g2i);
+            const float gam = __builtin_amdgcn_exp2f(g2i);
             #pragma unroll
             for (int q = 0; q < 4; ++q) oa[q] = gam * (xh[q] + xl[q]);
         }
@@ -594,7 +594,7 @@ __device__ __forceinline__ void chain_role(const GdnParams& p, GdnSmem<DK>& sm, 
         }
         const float g2 = sm.tab[b][16 * R + li], bt = sm.tab[b][CH + 16 * R + li];
         const float g2l = sm.tab[b][CH - 1];
-        const float gam = exp2f(g2), wm = exp2f(g2l - g2), gl = exp2f(g2l);
+        const float gam = __builtin_amdgcn_exp2f(g2), wm = __builtin_amdgcn_exp2f(g2l - g2), gl = __builtin_amdgcn_exp2f(g2l);
         const uint32_t v0 = cur.v[0], v1 = cur.v[1];
         const float vv[4] = {f32_of(v0 << 16), f32_of(v0 & 0xFFFF0000u), f32_of(v1 << 16), f32_of(v1 & 0xFFFF0000u)};
 

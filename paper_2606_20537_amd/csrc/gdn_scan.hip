@@ -369,27 +369,45 @@ __device__ __forceinline__ void out_role(const GdnParams& p, GdnSmem<DK>& sm, co
     // which forces nothing but the load's completion.
     constexpr int PREFETCH = 5;
     uint32_t pf[4] = {0u, 0u, 0u, 0u};
-    auto prefetch = [&](int slot, int64_t c) {
-        __asm__ volatile("" : : "v"(pf[slot]));
-        const int64_t t0 = c * CH;
-        const int rows = (int)chunk_rows(x, c);
+    // The lane's line, fixed for the call: kind 0 the workspace record,
+    // 1 K, 2 Q, 3 V, 4 none; its row in the chunk and byte offset in the row
+    // (or in the record).
+    int pkind = 4, prow = 0;
+    int64_t poff = 0;
+    if constexpr (R == 1 || R == 2) {
         const int ns = dv / DVS;
         const int L = j0 / DVS + ns * (64 * (R - 1) + lane);
         constexpr int LK = DK * 2 / 128;            // 128-byte lines per row of K or Q
         const int LV = (dv * 2 + 127) / 128;        // lines per row of the head's V
         constexpr int nR = (int)((kGdnWsRecord + 127) / 128);
         const int nK = CH * LK, nV = CH * LV;
-        const char* a = static_cast<const char*>(p.k);  // in bounds whenever the loop runs
         if (L < nR) {
-            if (c < x.n) a = reinterpret_cast<const char*>(p.ws) + (c * H + h) * kGdnWsRecord + L * 128;
+            pkind = 0;
+            poff = (int64_t)L * 128;
         } else if (L < nR + 2 * nK) {
             const int l = L - nR;
-            const int lq = l < nK ? l : l - nK, row = lq / LK;
-            if (row < rows)
-                a = static_cast<const char*>(l < nK ? p.k : p.q) + (t0 + row) * x.qk_row + h * DK * 2 + (lq % LK) * 128;
+            const int lq = l < nK ? l : l - nK;
+            pkind = l < nK ? 1 : 2;
+            prow = lq / LK;
+            poff = (int64_t)h * DK * 2 + (lq % LK) * 128;
         } else if (L < nR + 2 * nK + nV) {
-            const int l = L - nR - 2 * nK, row = l / LV;
-            if (row < rows) a = static_cast<const char*>(p.v) + (t0 + row) * x.v_row + h * dv * 2 + (l % LV) * 128;
+            const int l = L - nR - 2 * nK;
+            pkind = 3;
+            prow = l / LV;
+            poff = (int64_t)h * dv * 2 + (l % LV) * 128;
+        }
+    }
+    const char* const pbase = pkind == 1 ? static_cast<const char*>(p.k)
+                            : pkind == 2 ? static_cast<const char*>(p.q)
+                                         : static_cast<const char*>(p.v);
+    const int64_t prow_bytes = pkind == 3 ? x.v_row : x.qk_row;
+    auto prefetch = [&](int slot, int64_t c) {
+        __asm__ volatile("" : : "v"(pf[slot]));
+        const char* a = static_cast<const char*>(p.k);  // in bounds whenever the loop runs
+        if (pkind == 0) {
+            if (c < x.n) a = reinterpret_cast<const char*>(p.ws) + (c * H + h) * kGdnWsRecord + poff;
+        } else if (pkind < 4) {
+            if (prow < (int)chunk_rows(x, c)) a = pbase + (c * CH + prow) * prow_bytes + poff;
         }
         pf[slot] = *reinterpret_cast<const uint32_t*>(a);
     };

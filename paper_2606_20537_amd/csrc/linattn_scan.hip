@@ -204,7 +204,7 @@ __device__ inline uint32_t chunk_rows(const Ctx& x, int64_t c) {
 // chunk ahead of the V wave, which reads its weights from LDS.  Waves 5-7
 // share one instantiation: a separate one for the gate wave measured 10 %
 // slower with the same arithmetic.
-template <int DK, bool F32, bool ONE, bool VW>
+template <int DK, bool F32, bool ONE, bool CS, bool VW>
 __device__ __forceinline__ void state_role(const ScanParams& p, Smem<DK, F32>& sm, const Ctx& x, int wq) {
     const bool GW = !VW && wq == 1;  // wave-uniform
     using S_ = Smem<DK, F32>;
@@ -389,7 +389,8 @@ __device__ __forceinline__ void state_role(const ScanParams& p, Smem<DK, F32>& s
         pf[slot] = __builtin_amdgcn_raw_buffer_load_b32(r, tsel == 2 ? voff : qoff, 0, 0);
     };
 
-    // S_c as chunk state c (an empty buffer range when not wanted)
+    // S_c as chunk state c (an empty buffer range when not wanted: the
+    // one-chunk instance)
     auto store_state = [&](int64_t c, bool live) {
         const bool on = live && p.chunk_states != nullptr;
         const rsrc_t rc = make_rsrc_u32(p.chunk_states + (on ? c * (int64_t)H * DK * dv : 0),
@@ -433,7 +434,7 @@ __device__ __forceinline__ void state_role(const ScanParams& p, Smem<DK, F32>& s
         stage(Rs, u & 1, (u + 2) & 3);
         fold_delta((u + 1) & 1, Dn);
         const bool live = c < x.n;
-        store_state(c, live);
+        if constexpr (CS) store_state(c, live);
         if (live) advance(u, Dc);
         publish((u + 1) & 1);
         if (live) lds_barrier();
@@ -694,8 +695,11 @@ __device__ __forceinline__ void output_role(const ScanParams& p, Smem<DK, F32>& 
     }
 }
 
-// ONE: the call holds at most one chunk.
-template <int DK, bool F32, bool ONE>
+// ONE: the call holds at most one chunk.  CS: a multi-chunk call that
+// stores the chunk states; without them the state waves issue no
+// chunk-state stores at all (rather than stores to an empty range, whose
+// address work costs the final-state-only call about 4 %).
+template <int DK, bool F32, bool ONE, bool CS>
 __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
     __shared__ Smem<DK, F32> sm;
     const int tid = threadIdx.x;
@@ -734,16 +738,17 @@ __global__ __launch_bounds__(NT) void linattn_scan_kernel(const ScanParams p) {
         case 1: output_role<DK, F32, ONE, 1>(p, sm, x); break;
         case 2: output_role<DK, F32, ONE, 2>(p, sm, x); break;
         case 3: output_role<DK, F32, ONE, 3>(p, sm, x); break;
-        case 4: state_role<DK, F32, ONE, true>(p, sm, x, 0); break;
-        default: state_role<DK, F32, ONE, false>(p, sm, x, wave - 4); break;
+        case 4: state_role<DK, F32, ONE, CS, true>(p, sm, x, 0); break;
+        default: state_role<DK, F32, ONE, CS, false>(p, sm, x, wave - 4); break;
     }
 }
 
 template <int DK, bool F32>
 hipError_t launch_t(const ScanParams& p, hipStream_t stream) {
     const unsigned grid = (unsigned)(p.H * (p.dv / DVS));
-    const void* fn = p.T <= CH ? reinterpret_cast<const void*>(&linattn_scan_kernel<DK, F32, true>)
-                               : reinterpret_cast<const void*>(&linattn_scan_kernel<DK, F32, false>);
+    const void* fn = p.T <= CH ? reinterpret_cast<const void*>(&linattn_scan_kernel<DK, F32, true, true>)
+                     : p.chunk_states ? reinterpret_cast<const void*>(&linattn_scan_kernel<DK, F32, false, true>)
+                                      : reinterpret_cast<const void*>(&linattn_scan_kernel<DK, F32, false, false>);
     return launch_kernel(fn, dim3(grid), dim3(NT), p, stream);
 }
 

@@ -67,25 +67,25 @@ LINK_PEAK_GBS = 64.0         # host link, PCIe 5.0 x16, one direction
 LINATTN_SRC = "paper_2606_20537_amd/csrc/linattn_scan.hip"
 COPY_SRC = "paper_2606_20537_amd/csrc/capsule_copy.hip"
 GDN_SRC = "paper_2606_20537_amd/csrc/gdn_scan.hip"
-LINATTN_SHA = "9643aa1bd5851b4567d8a8cb75b2478d3cd82f4c4fd4f9b466160fd423b7031f"
+LINATTN_SHA = "6fa11d865ae9d32daf767bfbc0308e9304367b6fec92600806c6385fcc34d4d9"
 COPY_SHA = "3fe58e0a55a7b15d596057bce3dc33d9409338b3d9d5d137fddb7f8da5978430"
 GDN_SHA = "4cdea6657262021a85378f62e243eda289150d1bf653666fc2f29d5c485d6c54"
 MEASURED_TRAFFIC = {
-    "scan_cs": {"src": LINATTN_SRC, "sha256": LINATTN_SHA, "bytes": 1228528694},
-    "restore": {"src": COPY_SRC, "sha256": COPY_SHA, "bytes": 1763613408},
-    "snapshot": {"src": COPY_SRC, "sha256": COPY_SHA, "bytes": 1763693125},
-    "fork4": {"src": COPY_SRC, "sha256": COPY_SHA, "bytes": 4409914292},
-    "gather": {"src": COPY_SRC, "sha256": COPY_SHA, "bytes": 1009527990},
-    "gdn": {"src": GDN_SRC, "sha256": GDN_SHA, "bytes": 1617682467},
+    "scan_cs": {"src": LINATTN_SRC, "sha256": LINATTN_SHA, "bytes": 1228826037},
+    "restore": {"src": COPY_SRC, "sha256": COPY_SHA, "bytes": 1763625618},
+    "snapshot": {"src": COPY_SRC, "sha256": COPY_SHA, "bytes": 1763688951},
+    "fork4": {"src": COPY_SRC, "sha256": COPY_SHA, "bytes": 4409930338},
+    "gather": {"src": COPY_SRC, "sha256": COPY_SHA, "bytes": 1010166192},
+    "gdn": {"src": GDN_SRC, "sha256": GDN_SHA, "bytes": 1617845357},
 }
 
 # MFMA pipe busy from SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x GRBM_GUI_ACTIVE
 # / 8 XCDs), per scan launch on the 48-layer workload, with the same sha256
 # guard.  Summary and commands: profiles/hybrid48_scan_counters.md.
 MEASURED_MFMA_BUSY = {
-    "scan_cs": {"src": LINATTN_SRC, "sha256": LINATTN_SHA, "frac": 0.1563},
-    "scan_final": {"src": LINATTN_SRC, "sha256": LINATTN_SHA, "frac": 0.1841},
-    "gdn_scan": {"src": GDN_SRC, "sha256": GDN_SHA, "frac": 0.1739},
+    "scan_cs": {"src": LINATTN_SRC, "sha256": LINATTN_SHA, "frac": 0.1591},
+    "scan_final": {"src": LINATTN_SRC, "sha256": LINATTN_SHA, "frac": 0.1918},
+    "gdn_scan": {"src": GDN_SRC, "sha256": GDN_SHA, "frac": 0.1751},
 }
 
 

@@ -58,6 +58,13 @@ def test_hybrid48_layer_all_heads(orc):
           % (e["o"], e["s"], e["c"], e_elem))
     assert max(e.values()) <= PARITY_TOL
     assert max(e.values()) <= SPLIT_TOL
+    # the final-state-only call (the cold-prefill configuration bench.py
+    # times for TTFT) takes its own instantiation: same o and final state
+    o2 = torch.empty_like(o)
+    fs2 = torch.empty_like(fs)
+    cap.linattn_chunked_prefill(d["q"], d["k"], d["v"], d["g"], o2, final_state=fs2)
+    torch.cuda.synchronize()
+    assert torch.equal(o2, o) and torch.equal(fs2, fs)
 
 
 def test_hybrid48_gdn_layer_all_heads(orc):

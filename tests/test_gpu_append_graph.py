@@ -6,7 +6,9 @@ copy the capsule back, append the suffix -- recorded as ONE HIP graph for
 the hybrid8 workload (restore + 32 decode steps, each an append of the
 token's K/V rows and conv inputs plus six one-token scans) and replayed:
 every replay equals the eager cold path bit for bit, with eager work and
-synchronisations between the replays."""
+synchronisations between the replays; and the same with an unaligned
+boundary, where the graph also re-prefills the remainder past P' (both
+mixers)."""
 import numpy as np
 import pytest
 
@@ -113,6 +115,59 @@ def test_restore_then_decode_as_one_graph():
         got = _snapshot_of(warm)
         for l, (a, b) in enumerate(zip(got[0], ref[0])):
             assert torch.equal(a[P:F], b[P:F]), (replay, "o", l)
+        for kind, xs, ys in (("state", got[1], ref[1]), ("conv", got[2], ref[2])):
+            for l, (a, b) in enumerate(zip(xs, ys)):
+                assert torch.equal(a, b), (replay, kind, l)
+        for l, (a, b) in enumerate(zip(got[3], ref[3])):
+            assert torch.equal(a[:F], b[:F]), (replay, "kv", l)
+        assert bool(torch.isfinite(junk))
+
+
+@pytest.mark.parametrize("mixer", ["linattn", "gdn"])
+def test_restore_remainder_prefill_and_decode_as_one_graph(mixer):
+    """A boundary that is not chunk-aligned (P = 2111, P' = 2048): restore,
+    the chunked prefill of the remainder [P', P) in every linear layer with
+    its append, then 32 decode steps, recorded as ONE graph (§3 Algorithm 1:
+    restore, then re-prefill the tokens past the boundary and append) and
+    replayed with eager work between replays; every replay equals the eager
+    cold prefill of [0, P) plus the same decode steps, bit for bit (§5: the
+    restored state sits on a chunk boundary)."""
+    import torch
+    w = synth.get_config("hybrid8")
+    P, n_steps = 2111, w.continuation
+    Pa = (P // w.chunk) * w.chunk
+    F = P + n_steps
+    inputs = make_inputs(w, F, w.seed, mixer)
+    cold = HybridStack(w, F, inputs=inputs, mixer=mixer)
+    cold.prefill(0, P)
+    cold.decode(n_steps)
+    torch.cuda.synchronize()
+    ref = _snapshot_of(cold)
+    warm = HybridStack(w, F, inputs=inputs, mixer=mixer)
+    warm.prefill(0, Pa)
+    d = cap.capsule_digest_tokens(synth.token_ids(w.seed, P))
+    c = warm.snapshot(P, d)
+    warm.prefill(Pa, P)                        # the session went on past the boundary
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g, stream=side):
+            assert warm.restore(c, d) == Pa
+            warm.prefill(Pa, P)
+            warm.decode(n_steps)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    for replay in range(3):
+        warm.poison()
+        junk = torch.randn(1 << 20, device="cuda").sum()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got = _snapshot_of(warm)
+        for l, (a, b) in enumerate(zip(got[0], ref[0])):
+            assert torch.equal(a[Pa:F], b[Pa:F]), (replay, "o", l)
         for kind, xs, ys in (("state", got[1], ref[1]), ("conv", got[2], ref[2])):
             for l, (a, b) in enumerate(zip(xs, ys)):
                 assert torch.equal(a, b), (replay, kind, l)

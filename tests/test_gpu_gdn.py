@@ -63,6 +63,8 @@ CASES = [
     ("t63", 63, 2, 128, 48, True),
     ("t65", 65, 2, 128, 48, True),
     ("dk64_long", 1000, 2, 64, 32, True),
+    # 512 workgroups: more than one workgroup per CU over the call
+    ("h64_512_workgroups", 200, 64, 128, 128, True),
 ]
 
 

@@ -43,6 +43,8 @@ CASES = [
     ("f32_one_token", 1, 2, 64, 64, "f32", True),
     ("bf16_63", 63, 2, 128, 48, "bf16", True),
     ("bf16_65", 65, 2, 128, 48, "bf16", True),
+    # 16 slices per head, 512 workgroups: more than one workgroup per CU over the call
+    ("bf16_dv256_512_workgroups", 200, 32, 128, 256, "bf16", True),
 ]
 
 

@@ -296,3 +296,95 @@ def test_append_across_two_launches_matches_oracle(orc):
     for b, want in zip(bufs, host):
         assert np.array_equal(b[1].cpu().numpy(), want), b[0]
     assert cap.cap_set_get_position(s) == pos + n
+
+
+def _big_layout(n, seed):
+    """n buffers of mixed kinds and widths (positional rows of 16-80 B over
+    200 rows, fixed buffers of 16-272 B), in a seeded order."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        if rng.random() < 0.5:
+            out.append(("p%d" % i, 16 * int(rng.integers(1, 6)), 200, cap.CAP_KIND_POSITIONAL))
+        else:
+            out.append(("f%d" % i, 16 * int(rng.integers(1, 18)), 1, cap.CAP_KIND_FIXED))
+    return out
+
+
+def test_snapshot_restore_with_the_maximum_buffer_count(orc):
+    """A set of CAP_MAX_BUFFERS (512) buffers, the largest segment table a
+    copy block holds: snapshot bytes equal the oracle's, and restore after
+    poisoning rewrites exactly the capsule's bytes (rows past P' untouched)."""
+    import torch
+    layout = _big_layout(cap.CAP_MAX_BUFFERS, 1)
+    s, bufs = _make_set(60, layout)
+    P = 140
+    Pa = cap.cap_align_boundary(P, CHUNK)
+    cap.cap_set_set_position(s, Pa)
+    orig = _host(bufs)
+    rb, rt, kd = _lay(bufs)
+    nbytes = cap.capsule_bytes(s, P)
+    assert nbytes == orc.capsule_bytes(rb, rt, kd, Pa)
+    arena = device_bytes(nbytes)
+    c = cap.capsule_snapshot(s, P, 3, arena)
+    torch.cuda.synchronize()
+    assert np.array_equal(arena.cpu().numpy(), orc.snapshot(orig, rb, rt, kd, Pa))
+    for b in bufs:
+        b[1].fill_(0xA5)
+    assert cap.capsule_restore(c, s, 3) == Pa
+    torch.cuda.synchronize()
+    want = [np.full_like(o, 0xA5) for o in orig]
+    orc.restore(orc.snapshot(orig, rb, rt, kd, Pa), want, rb, rt, kd, Pa)
+    for got, w in zip(_host(bufs), want):
+        assert np.array_equal(got, w)
+
+
+def test_fork_to_the_maximum_destination_count_over_two_launches(orc):
+    """Fork into CAP_MAX_FORK (16) sets of 200 buffers: 3,200 destination
+    pointers exceed one launch's LDS table, so the call takes two launches;
+    every branch holds the capsule's bytes and nothing else changed."""
+    import torch
+    layout = _big_layout(200, 2)
+    src, bufs = _make_set(70, layout)
+    P = 128
+    cap.cap_set_set_position(src, P)
+    arena = device_bytes(cap.capsule_bytes(src, P))
+    c = cap.capsule_snapshot(src, P, 5, arena)
+    branches = [_make_set(80 + i, layout) for i in range(cap.CAP_MAX_FORK)]
+    before = [_host(bb) for _, bb in branches]
+    cap.capsule_fork(c, [b[0] for b in branches], 5)
+    torch.cuda.synchronize()
+    rb, rt, kd = _lay(bufs)
+    snap = orc.snapshot(_host(bufs), rb, rt, kd, P)
+    for (s, bb), old in zip(branches, before):
+        want = [o.copy() for o in old]
+        orc.restore(snap, want, rb, rt, kd, P)
+        for got, w in zip(_host(bb), want):
+            assert np.array_equal(got, w)
+        assert cap.cap_set_get_position(s) == P
+
+
+def test_gather_over_more_environments_than_one_launch(orc):
+    """70 environments from a gallery of 3 capsules: the call takes two
+    launches (64 + 6 environments); each environment holds its capsule's
+    bytes and nothing else changed."""
+    import torch
+    P = 64
+    gallery = []
+    for gi in range(3):
+        s, bufs = _make_set(90 + gi)
+        cap.cap_set_set_position(s, P)
+        arena = device_bytes(cap.capsule_bytes(s, P))
+        gallery.append((cap.capsule_snapshot(s, P, 0, arena), _host(bufs)))
+    envs = [_make_set(100 + e) for e in range(70)]
+    before = [_host(bb) for _, bb in envs]
+    ids = np.random.default_rng(9).integers(0, 3, size=70).astype(np.int32)
+    cap.capsule_gather_restore([g[0] for g in gallery], ids, [e[0] for e in envs])
+    torch.cuda.synchronize()
+    rb, rt, kd = _lay(envs[0][1])
+    for (s, bb), old, i in zip(envs, before, ids):
+        want = [o.copy() for o in old]
+        orc.restore(orc.snapshot(gallery[i][1], rb, rt, kd, P), want, rb, rt, kd, P)
+        for got, w in zip(_host(bb), want):
+            assert np.array_equal(got, w)
+        assert cap.cap_set_get_position(s) == P

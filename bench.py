@@ -67,7 +67,7 @@ LINK_PEAK_GBS = 64.0         # host link, PCIe 5.0 x16, one direction
 LINATTN_SRC = "paper_2606_20537_amd/csrc/linattn_scan.hip"
 COPY_SRC = "paper_2606_20537_amd/csrc/capsule_copy.hip"
 GDN_SRC = "paper_2606_20537_amd/csrc/gdn_scan.hip"
-LINATTN_SHA = "6fa11d865ae9d32daf767bfbc0308e9304367b6fec92600806c6385fcc34d4d9"
+LINATTN_SHA = "09e420c2db0aea75d4aceb67e34dbe75c35c7f6ed39eb054bbbfd048226ade63"
 COPY_SHA = "3fe58e0a55a7b15d596057bce3dc33d9409338b3d9d5d137fddb7f8da5978430"
 GDN_SHA = "4cdea6657262021a85378f62e243eda289150d1bf653666fc2f29d5c485d6c54"
 MEASURED_TRAFFIC = {

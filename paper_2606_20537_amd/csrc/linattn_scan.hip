@@ -186,7 +186,8 @@ __device__ inline uint32_t chunk_rows(const Ctx& x, int64_t c) {
 
 // Both roles walk the chunks four steps per loop iteration (the register
 // stages rotate without copies).  Every global access of a step is issued
-// unconditionally -- chunks past the end get an empty buffer range: loads
+// unconditionally (the chunk-state stores exist only in the instantiation
+// that writes chunk states) -- chunks past the end get an empty buffer range: loads
 // read zeros, stores are dropped -- so the compiler's in-order memory
 // counters stay exact and the prefetch is never drained; a step past the end
 // changes no state, writes only LDS buffers no live step reads, and skips

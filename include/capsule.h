@@ -127,7 +127,8 @@ CAP_API int capsule_layout_bytes(const cap_buf* bufs, uint32_t n, uint32_t chunk
  * deployment key (a digest of weights, quantisation, kernels and shape
  * bucket; restore refuses a capsule taken under another key, §3 Algorithm 1).
  * Checks: names unique when given, kinds known, pointers and row_bytes
- * 16-byte aligned, buffers pairwise disjoint.  Builds the static device
+ * 16-byte aligned, buffers pairwise disjoint, every buffer's address range
+ * and the sum of all buffer sizes within 64 bits (CAP_E_SIZE otherwise).  Builds the static device
  * segment table on the current device (one hipMalloc).  The set's position
  * starts at 0.  *out receives the handle. */
 CAP_API int cap_set_create(const cap_buf* bufs, uint32_t n, uint32_t chunk,

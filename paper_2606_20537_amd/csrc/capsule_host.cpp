@@ -118,13 +118,18 @@ int check_bufs(const cap_buf* bufs, uint32_t n, uint32_t chunk, bool need_ptr) {
     if (!bufs || n == 0) return CAP_E_INVAL;
     if (n > CAP_MAX_BUFFERS) return CAP_E_UNSUPPORTED;
     if (chunk == 0) return CAP_E_INVAL;
+    uint64_t total = 0;  // every byte count derived from the set stays below this sum
     for (uint32_t i = 0; i < n; ++i) {
         const cap_buf& b = bufs[i];
         if (b.kind != CAP_KIND_POSITIONAL && b.kind != CAP_KIND_FIXED) return CAP_E_UNSUPPORTED;
         if (b.reserved != 0) return CAP_E_INVAL;
         if (b.row_bytes == 0 || b.rows == 0) return CAP_E_INVAL;
         if (b.row_bytes > (UINT64_MAX / b.rows)) return CAP_E_SIZE;
+        const uint64_t size = b.row_bytes * b.rows;
+        if (size > UINT64_MAX - total) return CAP_E_SIZE;
+        total += size;
         if (need_ptr && !b.dptr) return CAP_E_INVAL;
+        if (need_ptr && (uint64_t)(uintptr_t)b.dptr > UINT64_MAX - size) return CAP_E_SIZE;  // range wraps
         if (!aligned16(b.row_bytes) || !aligned16((uint64_t)(uintptr_t)b.dptr)) return CAP_E_ALIGN;
     }
     // unique names (when given)

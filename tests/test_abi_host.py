@@ -93,6 +93,10 @@ def test_layout_errors():
     assert _status(cap.capsule_layout_bytes, _bufs(ok), 64, 128) == cap.CAP_E_SIZE  # P' = 128 > 100 rows
     many = [("b%d" % i, 16, 1, 1) for i in range(cap.CAP_MAX_BUFFERS + 1)]
     assert _status(cap.capsule_layout_bytes, _bufs(many), 1, 0) == cap.CAP_E_UNSUPPORTED
+    # sizes that fit 64 bits one by one but not in sum
+    half = [("a", 1 << 62, 2, 1), ("b", 1 << 62, 2, 1)]
+    assert _status(cap.capsule_layout_bytes, _bufs(half), 64, 0) == cap.CAP_E_SIZE
+    assert _status(cap.capsule_layout_bytes, _bufs(half[:1]), 64, 0) == cap.CAP_OK
 
 
 def test_set_create_rejects_before_device():
@@ -102,6 +106,8 @@ def test_set_create_rejects_before_device():
     assert _status(cap.cap_set_create, [("k", 4096, 64, 10, 3)], 64, 1) == cap.CAP_E_UNSUPPORTED
     overlapping = [("a", 4096, 64, 10, 0), ("b", 4096 + 320, 64, 10, 0)]
     assert _status(cap.cap_set_create, overlapping, 64, 1) == cap.CAP_E_INVAL
+    # an address range that wraps past 2^64
+    assert _status(cap.cap_set_create, [("k", (1 << 64) - 4096, 64, 100, 0)], 64, 1) == cap.CAP_E_SIZE
 
 
 def test_null_handles():
